@@ -1,0 +1,125 @@
+"""CPU oracle for the beam-search decode step (FastSeq, arXiv 2106.04718).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  It shares no
+code with the GPU library in ``paper_2106_04718_amd`` and never imports it.
+
+The arithmetic lives in ``oracle.c`` (plain C, fp64 for the attention); this
+module only marshals numpy arrays into it:
+
+* :func:`cross_attn` -- masked softmax(q K^T / sqrt(D)) V with one K/V copy
+  per source shared by its k beams (Appendix B, Eq. 4).
+* :func:`ngram_block` -- no-repeat-n-gram blocking as its definition
+  (Section 4.2, Algorithm 1): ban v iff (last n-1 tokens, v) already occurred.
+
+bf16 inputs are passed as their uint16 bit patterns and widened exactly to
+fp64 here (a bf16 value is the upper half of an fp32 value), so the oracle
+sees exactly the numbers the GPU reads.
+"""
+import ctypes
+import pathlib
+
+import numpy as np
+
+_HERE = pathlib.Path(__file__).resolve().parent
+_LIB = None
+
+_dp = ctypes.POINTER(ctypes.c_double)
+_fp = ctypes.POINTER(ctypes.c_float)
+_ip = ctypes.POINTER(ctypes.c_int32)
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        path = _HERE / "liboracle.so"
+        if not path.exists():
+            from . import build as _build
+            _build.build()
+        lib = ctypes.CDLL(str(path))
+        lib.oracle_cross_attn.argtypes = [_dp, _dp, _dp, _ip, _dp] + [ctypes.c_int] * 5
+        lib.oracle_cross_attn.restype = ctypes.c_int
+        lib.oracle_ngram_block.argtypes = [_ip, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_int, _fp, ctypes.c_int]
+        lib.oracle_ngram_block.restype = ctypes.c_int
+        lib.oracle_num_threads.argtypes = []
+        lib.oracle_num_threads.restype = ctypes.c_int
+        lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_num_threads.restype = None
+        _LIB = lib
+    return _LIB
+
+
+def widen(x: np.ndarray) -> np.ndarray:
+    """Exact fp64 copy of an fp32/fp64 array or of bf16 bits stored as uint16."""
+    x = np.asarray(x)
+    if x.dtype == np.uint16:
+        return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    if x.dtype in (np.float32, np.float64):
+        return x.astype(np.float64)
+    raise TypeError(f"unsupported input dtype {x.dtype}")
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    _lib().oracle_set_num_threads(int(n))
+
+
+def cross_attn(q, K, V, src_len) -> np.ndarray:
+    """fp64 encoder-decoder attention over de-duplicated K/V (Eq. 4).
+
+    q [B,k,H,D]; K, V [B,H,S,D] (fp32, fp64, or bf16 bits as uint16);
+    src_len [B] int32 (clamped to [0, S]).  Returns out [B,k,H,D] fp64.
+    """
+    qd = np.ascontiguousarray(widen(q))
+    Kd = np.ascontiguousarray(widen(K))
+    Vd = np.ascontiguousarray(widen(V))
+    return cross_attn_f64(qd, Kd, Vd, src_len)
+
+
+def cross_attn_f64(q, K, V, src_len) -> np.ndarray:
+    """As :func:`cross_attn` but takes contiguous fp64 arrays as they are."""
+    if q.ndim != 4 or K.ndim != 4 or V.shape != K.shape:
+        raise ValueError("q must be [B,k,H,D] and K, V [B,H,S,D]")
+    B, k, H, D = q.shape
+    if K.shape[0] != B or K.shape[1] != H or K.shape[3] != D:
+        raise ValueError(f"shape mismatch q{q.shape} K{K.shape}")
+    S = K.shape[2]
+    for a in (q, K, V):
+        if a.dtype != np.float64 or not a.flags.c_contiguous:
+            raise ValueError("cross_attn_f64 takes contiguous fp64 arrays")
+    lens = np.ascontiguousarray(np.asarray(src_len, dtype=np.int32))
+    if lens.shape != (B,):
+        raise ValueError("src_len must be [B]")
+    out = np.empty((B, k, H, D), dtype=np.float64)
+    rc = _lib().oracle_cross_attn(
+        q.ctypes.data_as(_dp), K.ctypes.data_as(_dp), V.ctypes.data_as(_dp),
+        lens.ctypes.data_as(_ip), out.ctypes.data_as(_dp), B, k, H, S, D)
+    if rc != 0:
+        raise ValueError("oracle_cross_attn rejected its arguments")
+    return out
+
+
+def ngram_block(tokens, n: int, logits, t: int | None = None) -> np.ndarray:
+    """Return a copy of ``logits`` with no-repeat-n-gram bans applied.
+
+    tokens [rows, ld] int32 (the first ``t`` columns are the history,
+    default ``t = ld``); logits [rows, V] fp32.  Banned entries become -inf;
+    all others are returned bit for bit.
+    """
+    tok = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    lg = np.array(logits, dtype=np.float32, copy=True, order="C")
+    if tok.ndim != 2 or lg.ndim != 2 or tok.shape[0] != lg.shape[0]:
+        raise ValueError("tokens must be [rows, ld] and logits [rows, V]")
+    rows, ld = tok.shape
+    if t is None:
+        t = ld
+    rc = _lib().oracle_ngram_block(tok.ctypes.data_as(_ip), ld, rows, int(t), int(n),
+                                   lg.ctypes.data_as(_fp), lg.shape[1])
+    if rc != 0:
+        raise ValueError("oracle_ngram_block rejected its arguments")
+    return lg

@@ -1,0 +1,186 @@
+/*
+ * CPU oracle for the beam-search decode step of FastSeq (arXiv 2106.04718).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load or run this code.  It shares no code,
+ * header, table or helper with the GPU library, and the GPU library never
+ * calls it.
+ *
+ * It is deliberately plain: straight loops in the order of the definitions,
+ * fp64 arithmetic for the attention, and no blocking, fusion or reordering.
+ * OpenMP only spreads independent output rows over threads; each row is
+ * computed by one thread in a fixed order, so the result does not depend on
+ * the thread count.
+ *
+ *   oracle_cross_attn   encoder-decoder attention over a de-duplicated K/V
+ *                       cache (Appendix B, Eq. 4), with a key-length mask.
+ *   oracle_ngram_block  no-repeat-n-gram blocking (Section 4.2, Algorithm 1)
+ *                       written as its plain definition.
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/*
+ * Encoder-decoder attention with de-duplicated K/V (Appendix B, Eq. 4).
+ *
+ * Eq. 4 keeps one copy of the encoder keys and values per source,
+ * Cache_K / Cache_V of shape [B, 1, N, D], and lets the B*M beam queries of
+ * step t read it through an einsum; the result is the attention line of
+ * Eq. 1, softmax(Q K^T / sqrt(d_k)) V, with K and V shared by the beams of a
+ * source.  Written per head: every (source b, beam i, head h) is an
+ * independent single-query attention over the keys of source b.
+ *
+ * Layouts (row-major, contiguous):
+ *   q       [B, k, H, D]   query of beam i of source b (hypothesis b*k + i)
+ *   K, V    [B, H, S, D]   one copy per source; rows j >= len are padding
+ *   src_len [B]            valid keys of source b; clamped to [0, S]
+ *   out     [B, k, H, D]
+ *
+ * Readings where the paper is silent: keys j >= src_len[b] take no weight
+ * (they are never read); the scale 1/sqrt(D) multiplies the scores; the
+ * softmax subtracts the row maximum, which leaves it unchanged
+ * mathematically; an empty key set (len 0) gives a zero output row.
+ *
+ * Returns 0, or 1 for invalid sizes (nothing is written then).
+ */
+int oracle_cross_attn(const double *q, const double *K, const double *V,
+                      const int32_t *src_len, double *out,
+                      int B, int k, int H, int S, int D)
+{
+    if (B < 0 || k < 0 || H < 0 || S < 0 || D < 1)
+        return 1;
+    if (B == 0 || k == 0 || H == 0)
+        return 0;
+    if (!q || !K || !V || !src_len || !out)
+        return 1;
+
+    const double root_d = sqrt((double)D);
+    const long rows = (long)B * k * H;
+
+#pragma omp parallel for schedule(dynamic, 4)
+    for (long r = 0; r < rows; ++r) {
+        /* r = (b*k + i)*H + h: source b, beam i, head h */
+        const int h = (int)(r % H);
+        const int b = (int)(r / ((long)H * k));
+        const double *qrow = q + r * D;  /* q[b, i, h, :] */
+        double *orow = out + r * D;      /* out[b, i, h, :] */
+        const double *Kbh = K + ((size_t)b * H + h) * (size_t)S * D;
+        const double *Vbh = V + ((size_t)b * H + h) * (size_t)S * D;
+
+        int L = src_len[b];
+        if (L < 0) L = 0;
+        if (L > S) L = S;
+        if (L == 0) {
+            for (int d = 0; d < D; ++d) orow[d] = 0.0;
+            continue;
+        }
+
+        double *w = (double *)malloc(sizeof(double) * (size_t)L);
+        if (!w) abort();
+
+        /* scores: s_j = (q . K_j) / sqrt(D) */
+        for (int j = 0; j < L; ++j) {
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d)
+                dot += qrow[d] * Kbh[(size_t)j * D + d];
+            w[j] = dot / root_d;
+        }
+        /* softmax over the valid keys */
+        double m = w[0];
+        for (int j = 1; j < L; ++j)
+            if (w[j] > m) m = w[j];
+        double Z = 0.0;
+        for (int j = 0; j < L; ++j) {
+            w[j] = exp(w[j] - m);
+            Z += w[j];
+        }
+        /* weighted sum of the values */
+        for (int d = 0; d < D; ++d) {
+            double acc = 0.0;
+            for (int j = 0; j < L; ++j)
+                acc += w[j] * Vbh[(size_t)j * D + d];
+            orow[d] = acc / Z;
+        }
+        free(w);
+    }
+    return 0;
+}
+
+/*
+ * No-repeat-n-gram blocking (Section 4.2, Algorithm 1; Section 2.2).
+ *
+ * Definition: for hypothesis row r with generated tokens x_0 .. x_{t-1},
+ * token v is banned iff the n-gram (x_{t-n+1}, .., x_{t-1}, v) already
+ * occurs in the row, i.e. there is a window start j in [0, t-n] with
+ * x_{j+c} == x_{t-n+1+c} for c = 0 .. n-2 and x_{j+n-1} == v.  A banned
+ * token's logit is set to -inf (zero probability); every other logit is
+ * left as it was.
+ *
+ * Readings: each window makes n-1 comparisons (the printed loop bound would
+ * read one token past the row); the last window may overlap the trailing
+ * n-1 tokens; token ids outside [0, V) are compared but never written;
+ * t < n gives no window and changes nothing; n == 1 bans every token of
+ * the row.
+ *
+ * Layouts: tokens [rows, ld] int32 (first t columns used), logits
+ * [rows, V] fp32, modified in place.
+ * Returns 0, or 1 for invalid arguments (nothing is written then).
+ */
+int oracle_ngram_block(const int32_t *tokens, int ld, int rows, int t, int n,
+                       float *logits, int V)
+{
+    if (rows < 0 || t < 0 || n < 1 || V < 0 || ld < t)
+        return 1;
+    if (rows == 0 || t < n)
+        return 0;
+    if (!tokens || !logits)
+        return 1;
+
+#pragma omp parallel for schedule(static)
+    for (int r = 0; r < rows; ++r) {
+        const int32_t *x = tokens + (size_t)r * ld;
+        float *lg = logits + (size_t)r * V;
+        const int suffix = t - n + 1; /* first of the trailing n-1 tokens */
+        for (int j = 0; j <= t - n; ++j) {
+            int same = 1;
+            for (int c = 0; c < n - 1; ++c) {
+                if (x[j + c] != x[suffix + c]) {
+                    same = 0;
+                    break;
+                }
+            }
+            if (!same)
+                continue;
+            const int32_t v = x[j + n - 1];
+            if (v >= 0 && v < V)
+                lg[v] = -INFINITY;
+        }
+    }
+    return 0;
+}
+
+/* Number of OpenMP threads a parallel region of the oracle uses. */
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* Set the OpenMP thread count for later calls (n >= 1). */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
