@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of the beam-search decode step on one MI355X.
+
+One step = the whole hot path on one batch: fs_beam_cross_attn (the k beams
+of every source read its one de-duplicated K/V copy) followed by
+fs_ngram_block on the step's logits, back to back on one stream.  Inputs are
+seeded synthetic BART-large-shaped tensors (workloads.py), resident in HBM
+before timing starts.  Each step reads a different K/V set, rotating over at
+least 1 GiB of sets so that the 256 MB last-level cache cannot hold them.
+
+Prints ONE JSON line:
+  value        algorithmic bytes of the step / step time (GB/s)
+  ms_per_step  mean step time over the timed steps (events around the region)
+  roofline     the cross-attention kernel's algorithmic GB/s against 8 TB/s,
+               from HIP events recorded around every launch in the timed
+               region (on the stream the kernels run on)
+  cpu_baseline the CPU oracle on the host cores, on the same inputs
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import pathlib
+import sys
+import time
+
+ROOT = pathlib.Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="bart", help="tiny | bart | t5 | prophetnet | large")
+    ap.add_argument("--rotate-gib", type=float, default=1.0,
+                    help="minimum total size of the rotated K/V sets")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-reps", type=int, default=0,
+                    help="oracle repetitions for the CPU baseline (0: until ~10 s)")
+    ap.add_argument("--copy-calibrate", type=float, default=0.0, metavar="GIB",
+                    help="instead of the step, run a plain device copy of this many GiB "
+                         "(reference for the FETCH_SIZE/WRITE_SIZE counters)")
+    ap.add_argument("--traffic", default=str(ROOT / "profiles" / "traffic.json"),
+                    help="HBM traffic per launch measured with rocprofv3 counters")
+    return ap.parse_args()
+
+
+def attn_bytes(cfg, lens) -> int:
+    """Algorithmic bytes of one cross-attention call: valid K and V rows,
+    q and out, and src_len.  Padding rows are never read."""
+    e = cfg.esize
+    kv = 2 * int(sum(int(x) for x in lens)) * cfg.H * cfg.D * e
+    qo = 2 * cfg.B * cfg.k * cfg.H * cfg.D * e
+    return kv + qo + 4 * cfg.B
+
+
+def ngram_bytes(rows: int, t: int, bans: int) -> int:
+    """Algorithmic bytes of one n-gram call: the token history is read once;
+    each banned logit is one 4-byte store (the logits are never read)."""
+    return rows * t * 4 + 4 * bans
+
+
+def copy_calibrate(gib: float) -> None:
+    import torch
+    n = int(gib * (1 << 30)) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the decode step shards by source with no exchange; see DESIGN.md)",
+              file=sys.stderr)
+        return 2
+    import numpy as np
+    import torch
+
+    from paper_2106_04718_amd import api, workloads
+
+    if args.copy_calibrate > 0:
+        copy_calibrate(args.copy_calibrate)
+        return 0
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    cfg = workloads.get(args.config)
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+
+    def dev_tensor(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    # ---- inputs, resident in HBM -----------------------------------------
+    t0 = time.perf_counter()
+    base = workloads.attn_inputs(cfg)
+    lens = base["src_len"]
+    set_bytes = 2 * cfg.B * cfg.H * cfg.S * cfg.D * cfg.esize
+    R = max(1, math.ceil(args.rotate_gib * (1 << 30) / set_bytes))
+    q = dev_tensor(base["q"])
+    lens_d = dev_tensor(lens)
+    Ks, Vs = [dev_tensor(base["K"])], [dev_tensor(base["V"])]
+    for r in range(1, R):
+        d = workloads.attn_inputs(cfg, rep=r)
+        Ks.append(dev_tensor(d["K"]))
+        Vs.append(dev_tensor(d["V"]))
+        del d
+    g = workloads.ngram_inputs(cfg)
+    tokens_d = dev_tensor(g["tokens"])
+    logits_d = dev_tensor(g["logits"])
+    out = torch.empty_like(q)
+    ws = torch.empty(max(16, api.beam_cross_attn_workspace_bytes(cfg.B, cfg.k, cfg.H, cfg.S, cfg.D, tdt)),
+                     dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    log(f"config={cfg.name} K/V sets={R} ({R * set_bytes / 2**30:.2f} GiB) inputs ready in "
+        f"{time.perf_counter() - t0:.1f}s")
+
+    def step(i: int):
+        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
+        api.ngram_block(tokens_d, cfg.n, logits_d)
+
+    # ---- first step: outputs kept for the CPU-baseline comparison ---------
+    api.beam_cross_attn(q, Ks[0], Vs[0], lens_d, out=out, workspace=ws)
+    api.ngram_block(tokens_d, cfg.n, logits_d)
+    torch.cuda.synchronize()
+    out0 = out.float().cpu().numpy().astype(np.float64)
+    logits0 = logits_d.cpu().numpy()
+    bans = int(np.isneginf(logits0).sum())
+
+    # ---- warm-up and timed region -----------------------------------------
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    K_ = args.steps
+    stream = torch.cuda.current_stream(dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K_)]
+    e_start = torch.cuda.Event(enable_timing=True)
+    e_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    e_start.record(stream)
+    for i in range(K_):
+        ev[i][0].record(stream)
+        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
+        ev[i][1].record(stream)
+        api.ngram_block(tokens_d, cfg.n, logits_d)
+        ev[i][2].record(stream)
+    e_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    region_ms = e_start.elapsed_time(e_end)
+    ca_us = np.array([ev[i][0].elapsed_time(ev[i][1]) * 1e3 for i in range(K_)])
+    ng_us = np.array([ev[i][1].elapsed_time(ev[i][2]) * 1e3 for i in range(K_)])
+    ms_per_step = region_ms / K_
+    b_ca = attn_bytes(cfg, lens)
+    b_ng = ngram_bytes(cfg.rows, cfg.t, bans)
+    b_step = b_ca + b_ng
+    value = b_step / (ms_per_step * 1e-3) / 1e9
+    ca_gbps = b_ca / (ca_us.mean() * 1e-6) / 1e9
+    log(f"step {ms_per_step * 1e3:.2f} us (wall {wall / K_ * 1e6:.2f} us); cross-attn "
+        f"{ca_us.mean():.2f} us (p10 {np.percentile(ca_us, 10):.2f}, p90 {np.percentile(ca_us, 90):.2f}) "
+        f"= {ca_gbps:.0f} GB/s; n-gram {ng_us.mean():.2f} us = {100 * ng_us.mean() / (ca_us.mean() + ng_us.mean()):.1f}% of step")
+
+    traffic = None
+    tp = pathlib.Path(args.traffic)
+    if tp.exists():
+        try:
+            rec = json.loads(tp.read_text()).get(cfg.name)
+            if rec and rec.get("kernel_source_sha") == kernel_source_sha():
+                traffic = rec.get("bytes_per_launch")
+        except (ValueError, OSError):
+            traffic = None
+
+    line = {
+        "metric": "decode-step µs and achieved HBM GB/s (cross-attn + n-gram block), BART-large shape",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K_,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "step_us": round(ms_per_step * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded; BART-large-shaped K/V, Zipf(1.1) token prefixes)",
+        "config": {"workload": workload_name(cfg), "B": cfg.B, "k": cfg.k, "H": cfg.H, "D": cfg.D,
+                   "S": cfg.S, "t": cfg.t, "V": cfg.V, "n": cfg.n, "kv_sets_rotated": R,
+                   "bytes_per_step": b_step},
+        "cross_attn_us": round(float(ca_us.mean()), 3),
+        "ngram_us": round(float(ng_us.mean()), 3),
+        "ngram_share_of_step": round(float(ng_us.mean() / (ca_us.mean() + ng_us.mean())), 4),
+        "roofline": {"bound": "hbm", "kernel": "fs_beam_cross_attn", "achieved": round(ca_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ca_gbps / HBM_PEAK_GBPS, 4),
+                     "algorithmic_bytes_per_launch": b_ca, "traffic": traffic},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"], line["parity"] = cpu_baseline(cfg, base, g, out0, logits0, b_step,
+                                                             args.cpu_reps)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def workload_name(cfg) -> str:
+    return (f"{cfg.name}-shaped decode step: cross-attn B={cfg.B} k={cfg.k} H={cfg.H} D={cfg.D} "
+            f"S={cfg.S} (lengths U{{{cfg.len_lo}..{cfg.len_hi}}}) {cfg.dtype} + no-repeat-{cfg.n}-gram "
+            f"on [{cfg.rows}, {cfg.t}] tokens, V={cfg.V}")
+
+
+def kernel_source_sha() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for p in sorted((ROOT / "paper_2106_04718_amd" / "csrc").glob("*")):
+        h.update(p.read_bytes())
+    return h.hexdigest()[:16]
+
+
+def cpu_baseline(cfg, base, g, out0, logits0, step_bytes, reps):
+    """The oracle, as it is, on the host cores: the same step on the same
+    inputs (K/V set 0).  Its outputs are also compared with the GPU's first step."""
+    import numpy as np
+
+    import oracle
+
+    qd, Kd, Vd = (np.ascontiguousarray(oracle.widen(base[x])) for x in ("q", "K", "V"))
+    tokens = np.ascontiguousarray(g["tokens"])
+    cores = oracle.num_threads()
+    times = []
+    ref = None
+    while True:
+        lg = np.array(g["logits"], copy=True)
+        t0 = time.perf_counter()
+        ref = oracle.cross_attn_f64(qd, Kd, Vd, base["src_len"])
+        oracle.ngram_block_inplace(tokens, cfg.n, lg, cfg.t)
+        times.append(time.perf_counter() - t0)
+        if (reps and len(times) >= reps) or (not reps and (sum(times) > 10.0 or len(times) >= 50)):
+            break
+    sec = float(np.median(times))
+    err = float(np.max(np.abs(out0 - ref)))
+    tol = 2e-2 if cfg.dtype == "bf16" else 1e-5 * float(np.max(np.abs(ref)))
+    ng_ok = bool(np.array_equal(lg.view(np.uint32), logits0.view(np.uint32)))
+    log(f"oracle: {sec * 1e3:.1f} ms per step on {cores} threads ({len(times)} reps); "
+        f"attn max abs err {err:.3e} (tol {tol:.1e}); n-gram bit-exact {ng_ok}")
+    cpu = {"value": round(step_bytes / sec / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
+           "sample": f"whole {cfg.name}-shaped step (all {cfg.B} sources x {cfg.k} beams x {cfg.H} heads, "
+                     f"{cfg.rows} token rows), K/V set 0, median of {len(times)} reps, "
+                     f"{sec * 1e3:.1f} ms per step"}
+    parity = {"attn_max_abs_err": err, "attn_tol": tol, "attn_ok": err <= tol, "ngram_bitexact": ng_ok}
+    return cpu, parity
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,141 @@
+/*
+ * fastseq_hip.h -- C ABI of the MI355X (gfx950) beam-search decode step.
+ *
+ * Two operations of FastSeq (arXiv 2106.04718) on one GPU:
+ *
+ *   fs_beam_cross_attn  encoder-decoder attention in which the k beam
+ *                       queries of a source read that source's single,
+ *                       de-duplicated K/V copy (Section 4.1.2; Appendix B,
+ *                       Eq. 4).
+ *   fs_ngram_block      no-repeat-n-gram blocking on the GPU (Section 4.2,
+ *                       Algorithm 1): logits of tokens that would repeat an
+ *                       earlier n-gram become -inf, in place.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named "device" are HIP device memory; the caller owns every
+ *     buffer.  The library never allocates, frees or synchronises in these
+ *     calls; it only enqueues kernels on `stream` (a hipStream_t; NULL means
+ *     the default stream) and returns.  A kernel fault surfaces at the
+ *     caller's next synchronisation.
+ *   - Arrays are row-major and contiguous unless a leading dimension is
+ *     passed.
+ *   - Argument errors are found on the host before any launch and leave all
+ *     outputs untouched.  The return value is an fs_status_t; its detail is
+ *     in fs_last_error().
+ *   - Calls are re-entrant; calls on different streams may run concurrently
+ *     as long as they do not share an output or workspace buffer.
+ *   - Debug mode: with the environment variable FS_VALIDATE=1 set when the
+ *     library is first used, fs_beam_cross_attn copies src_len to the host
+ *     (synchronising `stream`) and returns FS_ERR_INVALID_ARG if a length
+ *     lies outside [0, S] instead of clamping it.
+ */
+#ifndef FASTSEQ_HIP_H
+#define FASTSEQ_HIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FS_ABI_VERSION 1
+
+typedef enum {
+    FS_OK = 0,
+    FS_ERR_INVALID_ARG = 1,  /* bad pointer, size, alignment, aliasing or workspace */
+    FS_ERR_UNSUPPORTED = 2,  /* valid but not implemented: D, k or dtype outside the set below */
+    FS_ERR_HIP = 3           /* a HIP runtime call or kernel launch failed */
+} fs_status_t;
+
+typedef enum {
+    FS_F32 = 0,   /* IEEE binary32 */
+    FS_BF16 = 1   /* bfloat16 (upper half of a binary32) */
+} fs_dtype_t;
+
+/* FS_ABI_VERSION of the built library. */
+int fs_abi_version(void);
+
+/* Static name of a status code ("FS_OK", ...); "unknown status" otherwise. */
+const char *fs_status_string(int status);
+
+/* Detail of the status returned by the calling thread's last call into the
+ * library ("" if it returned FS_OK).  Owned by the library; valid until the
+ * thread's next call. */
+const char *fs_last_error(void);
+
+/*
+ * Workspace, in bytes, that fs_beam_cross_attn needs for these sizes
+ * (per-chunk softmax partials, fp32).  0 for empty problems; (size_t)-1 for
+ * invalid or unsupported sizes.  The size depends on every argument, so
+ * query it again whenever one changes.
+ */
+size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int dtype);
+
+/*
+ * Encoder-decoder attention over a de-duplicated K/V cache (Section 4.1.2;
+ * Appendix B, Eq. 4).
+ *
+ * For every source b, beam i < k and head h, with L = clamp(src_len[b], 0, S):
+ *     s_j          = (q[b,i,h,:] . K[b,h,j,:]) / sqrt(D)        for j < L
+ *     out[b,i,h,:] = sum_j softmax(s)_j * V[b,h,j,:]
+ * and out[b,i,h,:] = 0 when L == 0.  Rows j >= L of K and V are never read
+ * (they may hold anything, NaN included).  The k beams of source b are the
+ * hypotheses b*k .. b*k+k-1 of the flattened B*k batch; all of them read the
+ * one copy K[b], V[b], which is never replicated per beam.
+ *
+ * Arguments (all device pointers except the sizes):
+ *   q        [B, k, H, D]  dtype    queries of step t
+ *   K, V     [B, H, S, D]  dtype    encoder keys/values, one copy per source
+ *   src_len  [B]           int32    valid keys per source (right padding)
+ *   out      [B, k, H, D]  dtype    result, rounded to nearest-even from fp32
+ *   workspace, workspace_bytes      fp32 scratch of at least
+ *            fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype)
+ *            bytes; contents on entry do not matter and are clobbered.
+ *   stream   hipStream_t (NULL = default stream)
+ * Supported: dtype FS_F32 or FS_BF16, D in {16, 32, 64, 128}, 1 <= k <= 8,
+ * B, H, S >= 0 with B*k*H and B*H*ceil(S/256) below 2^31.
+ * Arithmetic: products and sums in fp32; the result does not depend on k,
+ * B or the beam's position (bitwise), only on (L, S, D, dtype) and the data.
+ * Errors: FS_ERR_INVALID_ARG for a null pointer with non-empty sizes,
+ * negative sizes, a pointer of q/K/V/out/workspace not 16-byte aligned, a
+ * workspace that is too small, or out or the workspace overlapping another
+ * argument; sizes too large for one launch;
+ * FS_ERR_UNSUPPORTED for D, k or dtype outside the set above; FS_ERR_HIP for
+ * a failed launch.  B == 0, k == 0 or H == 0 returns FS_OK with no launch.
+ */
+int fs_beam_cross_attn(const void *q, const void *K, const void *V,
+                       const int32_t *src_len, void *out,
+                       int B, int k, int H, int S, int D, int dtype,
+                       void *workspace, size_t workspace_bytes,
+                       void *stream);
+
+/*
+ * No-repeat-n-gram blocking (Section 4.2, Algorithm 1; Section 2.2).
+ *
+ * For every row r < rows with history x = tokens[r, 0..t-1]: if some window
+ * start j in [0, t-n] has x[j..j+n-2] == x[t-n+1..t-1] (the last n-1
+ * tokens), then logits[r, x[j+n-1]] = -inf.  Each window makes n-1
+ * comparisons; windows may overlap the last n-1 tokens.  Ids outside [0, V)
+ * take part in comparisons but are never written.  Every other logit keeps
+ * its bits.  Several windows banning one id write the same value.
+ *
+ * Arguments:
+ *   tokens     [rows, ld_tokens] int32, device; columns 0..t-1 are read
+ *   rows, t    hypotheses (B*k) and generated length; ld_tokens >= t
+ *   n          n-gram size, >= 1 (n == 1 bans every token of the row)
+ *   logits     [rows, V] fp32, device; modified in place
+ *   stream     hipStream_t (NULL = default stream)
+ * Errors: FS_ERR_INVALID_ARG for n < 1, negative sizes, ld_tokens < t,
+ * null pointers with non-empty sizes, or logits overlapping tokens;
+ * FS_ERR_HIP for a failed launch.  rows == 0 or t < n returns FS_OK with no
+ * launch.
+ */
+int fs_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t, int n,
+                   float *logits, int V, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASTSEQ_HIP_H */

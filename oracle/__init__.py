@@ -104,6 +104,21 @@ def cross_attn_f64(q, K, V, src_len) -> np.ndarray:
     return out
 
 
+def ngram_block_inplace(tokens: np.ndarray, n: int, logits: np.ndarray, t: int) -> None:
+    """As :func:`ngram_block` but writes into ``logits`` (contiguous float32)
+    and takes contiguous int32 ``tokens`` as they are (no copies)."""
+    if tokens.dtype != np.int32 or not tokens.flags.c_contiguous or tokens.ndim != 2:
+        raise ValueError("tokens must be contiguous int32 [rows, ld]")
+    if logits.dtype != np.float32 or not logits.flags.c_contiguous or logits.ndim != 2:
+        raise ValueError("logits must be contiguous float32 [rows, V]")
+    if tokens.shape[0] != logits.shape[0]:
+        raise ValueError("tokens and logits must have the same rows")
+    rc = _lib().oracle_ngram_block(tokens.ctypes.data_as(_ip), tokens.shape[1], tokens.shape[0],
+                                   int(t), int(n), logits.ctypes.data_as(_fp), logits.shape[1])
+    if rc != 0:
+        raise ValueError("oracle_ngram_block rejected its arguments")
+
+
 def ngram_block(tokens, n: int, logits, t: int | None = None) -> np.ndarray:
     """Return a copy of ``logits`` with no-repeat-n-gram bans applied.
 

@@ -1,0 +1,70 @@
+"""ctypes binding of libfastseq_hip.so (the C ABI declared in include/fastseq_hip.h).
+
+Only argument marshalling lives here.  The library must have been built
+(``__graft_entry__.build()`` or ``python -m paper_2106_04718_amd.build``);
+if it is missing every call raises -- there is no fallback path.
+"""
+import ctypes
+import pathlib
+
+_HERE = pathlib.Path(__file__).resolve().parent
+LIB_PATH = _HERE / "libfastseq_hip.so"
+
+FS_OK = 0
+FS_ERR_INVALID_ARG = 1
+FS_ERR_UNSUPPORTED = 2
+FS_ERR_HIP = 3
+FS_F32 = 0
+FS_BF16 = 1
+
+# (name, restype, argtypes) for every exported entry point.
+_c_int, _c_size, _vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
+SIGNATURES = [
+    ("fs_abi_version", _c_int, []),
+    ("fs_status_string", ctypes.c_char_p, [_c_int]),
+    ("fs_last_error", ctypes.c_char_p, []),
+    ("fs_beam_cross_attn_workspace_bytes", _c_size, [_c_int] * 6),
+    ("fs_beam_cross_attn", _c_int,
+     [_vp, _vp, _vp, _vp, _vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
+    ("fs_ngram_block", _c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp]),
+]
+
+_lib = None
+
+
+class NativeError(RuntimeError):
+    """A non-OK status from the library; ``status`` holds the fs_status_t."""
+
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{status_string(status)}: {detail}")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load the in-tree library once; raise if it was never built."""
+    global _lib
+    if _lib is None:
+        if not LIB_PATH.exists():
+            raise RuntimeError(
+                f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                "(no CPU fallback exists for the decode-step kernels)")
+        handle = ctypes.CDLL(str(LIB_PATH))
+        for name, res, args in SIGNATURES:
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().fs_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().fs_last_error().decode()
+
+
+def check(status: int) -> None:
+    if status != FS_OK:
+        raise NativeError(status, last_error())

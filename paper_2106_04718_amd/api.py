@@ -1,0 +1,107 @@
+"""Torch-tensor front end of the decode-step library.
+
+Each function checks tensor placement, dtype and layout, then passes raw
+device pointers and torch's current HIP stream to the C ABI.  PyTorch only
+provides memory and streams here; all arithmetic runs in the HIP kernels.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _native as N
+
+_DTYPES = {torch.float32: N.FS_F32, torch.bfloat16: N.FS_BF16}
+
+
+def _stream_ptr(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _need_cuda(name: str, t: torch.Tensor) -> None:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def beam_cross_attn_workspace_bytes(B: int, k: int, H: int, S: int, D: int,
+                                    dtype: torch.dtype = torch.bfloat16) -> int:
+    """Bytes of fp32 workspace fs_beam_cross_attn needs for these sizes."""
+    n = N.lib().fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, _DTYPES[dtype])
+    if n == 2**64 - 1:
+        raise N.NativeError(N.FS_ERR_UNSUPPORTED, N.last_error())
+    return int(n)
+
+
+def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: torch.Tensor,
+                    out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Encoder-decoder attention over de-duplicated K/V (Appendix B, Eq. 4).
+
+    q [B,k,H,D], K/V [B,H,S,D] (same dtype: float32 or bfloat16), src_len [B]
+    int32.  Returns out [B,k,H,D] in the input dtype.  ``workspace`` (uint8,
+    at least :func:`beam_cross_attn_workspace_bytes`) may be passed to avoid
+    an allocation per call.
+    """
+    for name, t in (("q", q), ("K", K), ("V", V), ("src_len", src_len)):
+        _need_cuda(name, t)
+    if q.dim() != 4 or K.dim() != 4 or K.shape != V.shape:
+        raise ValueError("q must be [B,k,H,D] and K, V [B,H,S,D]")
+    B, k, H, D = q.shape
+    if K.shape[0] != B or K.shape[1] != H or K.shape[3] != D:
+        raise ValueError(f"shape mismatch: q{tuple(q.shape)} K{tuple(K.shape)}")
+    S = K.shape[2]
+    if q.dtype not in _DTYPES or K.dtype != q.dtype or V.dtype != q.dtype:
+        raise ValueError("q, K and V must all be float32 or all bfloat16")
+    if src_len.dtype != torch.int32 or src_len.shape != (B,):
+        raise ValueError("src_len must be int32 [B]")
+    dev = q.device
+    if any(t.device != dev for t in (K, V, src_len)):
+        raise ValueError("all tensors must be on one device")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need_cuda("out", out)
+        if out.shape != q.shape or out.dtype != q.dtype or out.device != dev:
+            raise ValueError("out must match q in shape, dtype and device")
+    dt = _DTYPES[q.dtype]
+    need = beam_cross_attn_workspace_bytes(B, k, H, S, D, q.dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    else:
+        _need_cuda("workspace", workspace)
+    with torch.cuda.device(dev):
+        N.check(N.lib().fs_beam_cross_attn(
+            q.data_ptr(), K.data_ptr(), V.data_ptr(), src_len.data_ptr(), out.data_ptr(),
+            B, k, H, S, D, dt, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+            _stream_ptr(dev)))
+    return out
+
+
+def ngram_block(tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | None = None) -> torch.Tensor:
+    """No-repeat-n-gram blocking in place (Section 4.2, Algorithm 1).
+
+    tokens [rows, ld] int32 (row-contiguous; the first ``t`` columns are the
+    history, default all); logits [rows, V] float32, contiguous.  Returns
+    ``logits`` with banned entries set to -inf.
+    """
+    if not isinstance(tokens, torch.Tensor) or tokens.device.type != "cuda":
+        raise ValueError("tokens must be a GPU tensor")
+    _need_cuda("logits", logits)
+    if tokens.dim() != 2 or tokens.dtype != torch.int32 or tokens.stride(1) != 1:
+        raise ValueError("tokens must be int32 [rows, ld] with unit column stride")
+    if logits.dim() != 2 or logits.dtype != torch.float32:
+        raise ValueError("logits must be float32 [rows, V]")
+    rows = tokens.shape[0]
+    if logits.shape[0] != rows or logits.device != tokens.device:
+        raise ValueError("tokens and logits must have the same rows and device")
+    ld = tokens.stride(0) if rows > 1 else tokens.shape[1]
+    if t is None:
+        t = tokens.shape[1]
+    if t > tokens.shape[1]:
+        raise ValueError("t exceeds the columns of tokens")
+    dev = tokens.device
+    with torch.cuda.device(dev):
+        N.check(N.lib().fs_ngram_block(tokens.data_ptr(), ld, rows, int(t), int(n),
+                                       logits.data_ptr(), logits.shape[1], _stream_ptr(dev)))
+    return logits

@@ -1,0 +1,171 @@
+// C ABI of the decode-step library: argument validation, status codes and
+// dispatch to the kernels.  Every check here runs on the host before any HIP
+// call, so invalid arguments never reach the GPU and leave outputs untouched.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "fastseq_hip.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(FS_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// Do the byte ranges [a, a+na) and [b, b+nb) intersect?
+bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
+    if (na == 0 || nb == 0) return false;
+    const uintptr_t pa = reinterpret_cast<uintptr_t>(a), pb = reinterpret_cast<uintptr_t>(b);
+    return pa < pb + nb && pb < pa + na;
+}
+
+bool validate_mode() {
+    static const bool on = [] {
+        const char *v = std::getenv("FS_VALIDATE");
+        return v && v[0] == '1';
+    }();
+    return on;
+}
+
+bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
+
+// Host-side shape checks shared by the workspace query and the launch.
+// Returns FS_OK or an error status with g_last_error set.
+int check_attn_sizes(int B, int k, int H, int S, int D, int dtype) {
+    if (B < 0 || k < 0 || H < 0 || S < 0 || D < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (B=%d k=%d H=%d S=%d D=%d)", B, k, H, S, D);
+    if (dtype != FS_F32 && dtype != FS_BF16)
+        return fail(FS_ERR_UNSUPPORTED, "dtype %d is not FS_F32 or FS_BF16", dtype);
+    if (!supported_d(D)) return fail(FS_ERR_UNSUPPORTED, "head dim D=%d not in {16,32,64,128}", D);
+    if (k > 8) return fail(FS_ERR_UNSUPPORTED, "beam size k=%d > 8", k);
+    const int esize = dtype == FS_BF16 ? 2 : 4;
+    const long long C = fs::cross_attn_chunk_keys(D, esize);
+    const long long nc = (S + C - 1) / C;
+    if ((long long)B * k * H > INT_MAX || (long long)B * H * (nc > 0 ? nc : 1) > INT_MAX)
+        return fail(FS_ERR_INVALID_ARG, "problem too large for one launch (B=%d k=%d H=%d S=%d)",
+                    B, k, H, S);
+    return FS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fs_abi_version(void) { return FS_ABI_VERSION; }
+
+const char *fs_status_string(int status) {
+    switch (status) {
+    case FS_OK: return "FS_OK";
+    case FS_ERR_INVALID_ARG: return "FS_ERR_INVALID_ARG";
+    case FS_ERR_UNSUPPORTED: return "FS_ERR_UNSUPPORTED";
+    case FS_ERR_HIP: return "FS_ERR_HIP";
+    default: return "unknown status";
+    }
+}
+
+const char *fs_last_error(void) { return g_last_error.c_str(); }
+
+size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int dtype) {
+    g_last_error.clear();
+    if (check_attn_sizes(B, k, H, S, D, dtype) != FS_OK) return (size_t)-1;
+    if (B == 0 || k == 0 || H == 0) return 0;
+    const int esize = dtype == FS_BF16 ? 2 : 4;
+    return fs::cross_attn_workspace_floats(B, k, H, S, D, esize) * sizeof(float);
+}
+
+int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len,
+                       void *out, int B, int k, int H, int S, int D, int dtype,
+                       void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_last_error.clear();
+    int st = check_attn_sizes(B, k, H, S, D, dtype);
+    if (st != FS_OK) return st;
+    if (B == 0 || k == 0 || H == 0) return FS_OK;
+
+    const size_t esize = dtype == FS_BF16 ? 2 : 4;
+    const size_t q_bytes = (size_t)B * k * H * D * esize;
+    const size_t kv_bytes = (size_t)B * H * S * D * esize;
+    if (!q || !out || !src_len || (kv_bytes > 0 && (!K || !V)))
+        return fail(FS_ERR_INVALID_ARG, "null pointer (q=%p K=%p V=%p src_len=%p out=%p)",
+                    q, K, V, (const void *)src_len, out);
+    if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16))
+        return fail(FS_ERR_INVALID_ARG, "q, K, V and out must be 16-byte aligned");
+    if (!aligned(src_len, 4)) return fail(FS_ERR_INVALID_ARG, "src_len must be 4-byte aligned");
+    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, K, kv_bytes) ||
+        overlaps(out, q_bytes, V, kv_bytes) || overlaps(out, q_bytes, src_len, (size_t)B * 4))
+        return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
+    const size_t need = fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype);
+    if (workspace_bytes < need || (need > 0 && !workspace))
+        return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed",
+                    workspace_bytes, workspace, need);
+    if (!aligned(workspace, 16)) return fail(FS_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (need > 0 && (overlaps(workspace, need, q, q_bytes) || overlaps(workspace, need, K, kv_bytes) ||
+                     overlaps(workspace, need, V, kv_bytes) || overlaps(workspace, need, out, q_bytes) ||
+                     overlaps(workspace, need, src_len, (size_t)B * 4)))
+        return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (validate_mode()) {
+        std::vector<int32_t> lens((size_t)B);
+        hipError_t e = hipMemcpyAsync(lens.data(), src_len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "FS_VALIDATE copy of src_len");
+        for (int b = 0; b < B; ++b)
+            if (lens[b] < 0 || lens[b] > S)
+                return fail(FS_ERR_INVALID_ARG, "src_len[%d] = %d outside [0, %d]", b, lens[b], S);
+    }
+    hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
+                                         static_cast<float *>(workspace), s);
+    if (e != hipSuccess) return hip_fail(e, "fs_beam_cross_attn launch");
+    return FS_OK;
+}
+
+int fs_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t, int n,
+                   float *logits, int V, void *stream)
+{
+    g_last_error.clear();
+    if (rows < 0 || t < 0 || V < 0 || ld_tokens < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (rows=%d t=%d V=%d ld=%d)", rows, t, V, ld_tokens);
+    if (n < 1) return fail(FS_ERR_INVALID_ARG, "n=%d < 1", n);
+    if (ld_tokens < t) return fail(FS_ERR_INVALID_ARG, "ld_tokens=%d < t=%d", ld_tokens, t);
+    if (rows == 0 || t < n) return FS_OK;  // no window: nothing to ban
+    if (!tokens || (V > 0 && !logits))
+        return fail(FS_ERR_INVALID_ARG, "null pointer (tokens=%p logits=%p)", (const void *)tokens,
+                    (void *)logits);
+    if (!aligned(tokens, 4) || !aligned(logits, 4))
+        return fail(FS_ERR_INVALID_ARG, "tokens and logits must be 4-byte aligned");
+    const size_t tok_bytes = ((size_t)(rows - 1) * ld_tokens + t) * 4;
+    const size_t lg_bytes = (size_t)rows * V * 4;
+    if (overlaps(tokens, tok_bytes, logits, lg_bytes))
+        return fail(FS_ERR_INVALID_ARG, "logits overlap tokens");
+    if (V == 0) return FS_OK;  // no id is in range: nothing can be written
+    hipError_t e = fs::launch_ngram_block(tokens, ld_tokens, rows, t, n, logits, V,
+                                          static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "fs_ngram_block launch");
+    return FS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,29 @@
+// Internal launch interface between the C ABI (capi.cpp) and the kernels.
+// Arguments are already validated by the caller; these functions only size
+// the grid, enqueue the kernels on `stream` and return hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fs {
+
+// Keys per split-KV chunk of the cross-attention.  It depends only on the
+// row size (D and element size), never on B, k or the lengths, so the
+// reduction order -- and hence every output bit -- is the same whether a
+// source is read by one beam or by k beams.
+int cross_attn_chunk_keys(int D, int esize);
+
+// Number of fp32 values the per-chunk partials take for these sizes.
+size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize);
+
+hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
+                             const int32_t *src_len, void *out,
+                             int B, int k, int H, int S, int D, bool bf16,
+                             float *workspace, hipStream_t stream);
+
+hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t,
+                              int n, float *logits, int V, hipStream_t stream);
+
+}  // namespace fs

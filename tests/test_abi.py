@@ -1,0 +1,142 @@
+"""The C ABI loads without a GPU, exports what include/fastseq_hip.h declares,
+and rejects invalid arguments on the host before any HIP call.
+
+No test here launches a kernel: every call below fails validation (or is an
+empty problem) and returns before touching device memory, so the fake
+pointers passed are never dereferenced.
+"""
+import ctypes
+import pathlib
+import re
+
+import pytest
+
+from paper_2106_04718_amd import _native as N
+
+ROOT = pathlib.Path(__file__).resolve().parents[1]
+FAKE = 1 << 20          # aligned, never dereferenced
+
+
+def header_functions():
+    names = set()
+    for h in (ROOT / "include").glob("*.h"):
+        text = re.sub(r"/\*.*?\*/", "", h.read_text(), flags=re.S)
+        names.update(re.findall(r"\b(fs_[a-z0-9_]+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_function():
+    declared = header_functions()
+    assert {"fs_beam_cross_attn", "fs_ngram_block", "fs_beam_cross_attn_workspace_bytes",
+            "fs_abi_version", "fs_status_string", "fs_last_error"} <= declared
+    lib = ctypes.CDLL(str(N.LIB_PATH))
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert {s[0] for s in N.SIGNATURES} == declared
+
+
+def test_abi_version_and_status_strings():
+    lib = N.lib()
+    hdr = (ROOT / "include" / "fastseq_hip.h").read_text()
+    assert lib.fs_abi_version() == int(re.search(r"#define FS_ABI_VERSION (\d+)", hdr).group(1))
+    assert N.status_string(0) == "FS_OK"
+    assert N.status_string(1) == "FS_ERR_INVALID_ARG"
+    assert N.status_string(2) == "FS_ERR_UNSUPPORTED"
+    assert N.status_string(3) == "FS_ERR_HIP"
+    assert N.status_string(99) == "unknown status"
+
+
+def attn(**kw):
+    a = dict(q=FAKE, K=FAKE * 2, V=FAKE * 3, src_len=FAKE * 4, out=FAKE * 5,
+             B=2, k=4, H=2, S=64, D=16, dtype=N.FS_F32, ws=FAKE * 6, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return N.lib().fs_beam_cross_attn(a["q"], a["K"], a["V"], a["src_len"], a["out"], a["B"], a["k"],
+                                      a["H"], a["S"], a["D"], a["dtype"], a["ws"], a["ws_bytes"],
+                                      a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(B=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(S=-5), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(D=48), N.FS_ERR_UNSUPPORTED, "D=48"),
+    (dict(D=0), N.FS_ERR_UNSUPPORTED, "D=0"),
+    (dict(k=9), N.FS_ERR_UNSUPPORTED, "k=9"),
+    (dict(dtype=7), N.FS_ERR_UNSUPPORTED, "dtype"),
+    (dict(q=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(K=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(src_len=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(out=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(q=FAKE + 4), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(V=FAKE * 3 + 8), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(src_len=FAKE * 4 + 2), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(out=FAKE), N.FS_ERR_INVALID_ARG, "overlaps"),
+    (dict(out=FAKE * 2 + 64), N.FS_ERR_INVALID_ARG, "overlaps"),
+    (dict(ws_bytes=16), N.FS_ERR_INVALID_ARG, "workspace"),
+    (dict(ws=None), N.FS_ERR_INVALID_ARG, "workspace"),
+    (dict(ws=FAKE * 6 + 4), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(ws=FAKE * 3), N.FS_ERR_INVALID_ARG, "overlaps"),
+    (dict(B=1 << 20, H=1 << 12), N.FS_ERR_INVALID_ARG, "too large"),
+])
+def test_cross_attn_rejects(kw, status, needle):
+    assert attn(**kw) == status
+    assert needle in N.last_error()
+
+
+def test_cross_attn_empty_problems_return_ok_without_launch():
+    for kw in (dict(B=0), dict(k=0), dict(H=0)):
+        assert attn(q=None, K=None, V=None, src_len=None, out=None, ws=None, ws_bytes=0, **kw) == N.FS_OK
+        assert N.last_error() == ""
+
+
+def test_workspace_bytes():
+    f = N.lib().fs_beam_cross_attn_workspace_bytes
+    assert f(0, 4, 16, 1024, 64, N.FS_BF16) == 0
+    assert f(2, 4, 2, 0, 16, N.FS_F32) == 0                       # S = 0: no chunk
+    assert f(2, 4, 2, 64, 48, N.FS_F32) == 2**64 - 1
+    assert f(-1, 4, 2, 64, 16, N.FS_F32) == 2**64 - 1
+    # the size grows with every dimension and never with the padding beyond a chunk
+    a = f(32, 4, 16, 1024, 64, N.FS_BF16)
+    assert a > 0 and a % 16 == 0
+    assert f(64, 4, 16, 1024, 64, N.FS_BF16) == 2 * a
+    assert f(32, 8, 16, 1024, 64, N.FS_BF16) == 2 * a
+    assert f(32, 4, 16, 1025, 64, N.FS_BF16) > a
+    # per (b, h, chunk): k * (D + 2) fp32 values
+    assert a % (32 * 16 * 4 * 66 * 4) == 0
+
+
+def ngram(**kw):
+    a = dict(tokens=FAKE, ld=8, rows=4, t=8, n=3, logits=FAKE * 8, V=100, stream=None)
+    a.update(kw)
+    return N.lib().fs_ngram_block(a["tokens"], a["ld"], a["rows"], a["t"], a["n"], a["logits"],
+                                  a["V"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(n=0), N.FS_ERR_INVALID_ARG, "n=0"),
+    (dict(n=-2), N.FS_ERR_INVALID_ARG, "n=-2"),
+    (dict(rows=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(t=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(V=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(ld=4), N.FS_ERR_INVALID_ARG, "ld_tokens"),
+    (dict(tokens=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(logits=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(tokens=FAKE + 2), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(logits=FAKE + 64), N.FS_ERR_INVALID_ARG, "overlap"),
+])
+def test_ngram_rejects(kw, status, needle):
+    assert ngram(**kw) == status
+    assert needle in N.last_error()
+
+
+def test_ngram_no_window_returns_ok_without_launch():
+    # t < n and rows == 0 have no window; V == 0 leaves nothing writable
+    assert ngram(tokens=None, logits=None, t=2, n=3) == N.FS_OK
+    assert ngram(tokens=None, logits=None, rows=0) == N.FS_OK
+    assert ngram(logits=None, V=0) == N.FS_OK
+
+
+def test_validation_runs_before_any_hip_call():
+    # A rejected call must not initialise HIP (there is no GPU here): the
+    # status is the argument error, not FS_ERR_HIP.
+    assert attn(D=48) == N.FS_ERR_UNSUPPORTED
+    assert ngram(n=0) == N.FS_ERR_INVALID_ARG
