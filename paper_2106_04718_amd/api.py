@@ -88,8 +88,10 @@ def ngram_block(tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | Non
     if not isinstance(tokens, torch.Tensor) or tokens.device.type != "cuda":
         raise ValueError("tokens must be a GPU tensor")
     _need_cuda("logits", logits)
-    if tokens.dim() != 2 or tokens.dtype != torch.int32 or tokens.stride(1) != 1:
-        raise ValueError("tokens must be int32 [rows, ld] with unit column stride")
+    if tokens.dim() != 2 or tokens.dtype != torch.int32:
+        raise ValueError("tokens must be int32 [rows, ld]")
+    if tokens.numel() > 0 and tokens.shape[1] > 1 and tokens.stride(1) != 1:
+        raise ValueError("tokens must have unit column stride")
     if logits.dim() != 2 or logits.dtype != torch.float32:
         raise ValueError("logits must be float32 [rows, V]")
     rows = tokens.shape[0]
