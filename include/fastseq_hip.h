@@ -66,7 +66,8 @@ const char *fs_last_error(void);
 
 /*
  * Workspace, in bytes, that fs_beam_cross_attn needs for these sizes
- * (per-chunk softmax partials, fp32).  0 for empty problems; (size_t)-1 for
+ * (per-chunk softmax partials, fp32 values tagged with the call).  0 for
+ * empty problems; (size_t)-1 for
  * invalid or unsupported sizes.  The size depends on every argument, so
  * query it again whenever one changes.
  */
@@ -89,12 +90,15 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  *   K, V     [B, H, S, D]  dtype    encoder keys/values, one copy per source
  *   src_len  [B]           int32    valid keys per source (right padding)
  *   out      [B, k, H, D]  dtype    result, rounded to nearest-even from fp32
- *   workspace, workspace_bytes      fp32 scratch of at least
+ *   workspace, workspace_bytes      scratch of at least
  *            fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype)
- *            bytes; contents on entry do not matter and are clobbered.
+ *            bytes (per-chunk partials); its contents on entry do not
+ *            matter and are clobbered.  Calls that share a workspace must
+ *            not run concurrently.
  *   stream   hipStream_t (NULL = default stream)
  * Supported: dtype FS_F32 or FS_BF16, D in {16, 32, 64, 128}, 1 <= k <= 8,
- * B, H, S >= 0 with B*k*H and B*H*ceil(S/256) below 2^31.
+ * B, H, S >= 0 with B*k*H below 2^31 and a launch grid of about
+ * B*H*S*D*esize/8192 workgroups (esize = 2 or 4 bytes) below 2^31.
  * Arithmetic: products and sums in fp32; the result does not depend on k,
  * B or the beam's position (bitwise), only on (L, S, D, dtype) and the data.
  * Errors: FS_ERR_INVALID_ARG for a null pointer with non-empty sizes,

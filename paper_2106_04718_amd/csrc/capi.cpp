@@ -3,6 +3,8 @@
 // call, so invalid arguments never reach the GPU and leave outputs untouched.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <atomic>
 #include <climits>
 #include <cstdarg>
 #include <cstdint>
@@ -50,6 +52,17 @@ bool validate_mode() {
     return on;
 }
 
+// Epochs tag the cross-attention partial records in the workspace, so a
+// workspace never needs clearing: every call gets a fresh nonzero epoch.
+std::atomic<unsigned long long> g_epoch{1};
+
+unsigned long long next_epoch() {
+    for (;;) {
+        const unsigned long long e = g_epoch.fetch_add(1, std::memory_order_relaxed) & 0xffffffffull;
+        if (e != 0) return e;
+    }
+}
+
 bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
 
 // Host-side shape checks shared by the workspace query and the launch.
@@ -63,8 +76,9 @@ int check_attn_sizes(int B, int k, int H, int S, int D, int dtype) {
     if (k > 8) return fail(FS_ERR_UNSUPPORTED, "beam size k=%d > 8", k);
     const int esize = dtype == FS_BF16 ? 2 : 4;
     const long long C = fs::cross_attn_chunk_keys(D, esize);
-    const long long nc = (S + C - 1) / C;
-    if ((long long)B * k * H > INT_MAX || (long long)B * H * (nc > 0 ? nc : 1) > INT_MAX)
+    const long long nc = std::max(1LL, (S + C - 1) / C);
+    const long long bh_padded = ((long long)B * H + 7) / 8 * 8;  // chunk grid is padded to 8 XCDs
+    if ((long long)B * k * H > INT_MAX || bh_padded * nc + (long long)B * H > INT_MAX)
         return fail(FS_ERR_INVALID_ARG, "problem too large for one launch (B=%d k=%d H=%d S=%d)",
                     B, k, H, S);
     return FS_OK;
@@ -138,7 +152,7 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
                 return fail(FS_ERR_INVALID_ARG, "src_len[%d] = %d outside [0, %d]", b, lens[b], S);
     }
     hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
-                                         static_cast<float *>(workspace), s);
+                                         static_cast<float *>(workspace), next_epoch(), s);
     if (e != hipSuccess) return hip_fail(e, "fs_beam_cross_attn launch");
     return FS_OK;
 }

@@ -3,30 +3,38 @@
 // The operation is Eq. 4 of the paper (Appendix B): the k beam queries of
 // source b read the one copy K[b], V[b] of that source's encoder keys and
 // values, and each computes softmax(q K^T / sqrt(D)) V over the valid keys
-// j < src_len[b].  Per head it is a GEMV-like contraction with k query rows,
-// so it is bound by HBM bandwidth (about k flop per byte of K/V); the design
-// goal is to read every valid K/V byte exactly once, coalesced, and to keep
-// the VALU work per byte small enough to stay under the memory time.
+// j < src_len[b].  Per head it is a GEMV-like contraction with k query rows
+// (about k flop per byte of K/V), so it is bound by HBM bandwidth.  The
+// kernel reads every valid K/V byte exactly once with coalesced,
+// non-temporal 16-byte loads and keeps all k beams' work on that data in
+// registers.
 //
-// Work split (split-KV):
-//   kernel 1, one workgroup per (source b, head h, chunk c of C keys):
-//     Each of the 4 waves owns one tile of 64 consecutive keys of the chunk.
-//     QK^T:  lane j of the wave holds key j's whole row and forms the k
-//            scores itself (no cross-lane reduction); the k queries sit in
-//            LDS and are read as broadcasts.
-//     softmax: the tile's maximum and sum per beam are wave reductions, so
-//            every exponential is taken once per (key, beam).
-//     PV:    the weights go through LDS to a coalesced layout in which a
-//            group of lanes shares one V row (16 bytes per lane) and each lane
-//            accumulates k x (its 16 bytes of dims) in fp32.
-//     The four tiles are merged in fixed order and the chunk's partial
-//     (max, sum, unnormalised output) is written to the workspace.
-//   kernel 2, one workgroup per (b, h): merges the chunks of the source in
-//     order by log-sum-exp, normalises, rounds and stores.
+// One launch, split-KV:
+//   One workgroup per (source b, head h, chunk c of C keys); 4 waves, each
+//   owning one tile of the chunk.  In a tile a group of kLpr lanes shares one
+//   row (16 bytes per lane), so a wave instruction reads kRpi whole rows.
+//     QK^T:  each lane dots its 16 bytes of the row with the same 16 bytes of
+//            every beam's query (held in registers); a butterfly inside the
+//            lane group completes the k scores.
+//     softmax: tile maximum and sum per beam by cross-group butterflies; the
+//            running (max, sum) of the online softmax is wave-uniform.
+//     PV:    the same lane layout reads V; each lane accumulates k x (its 16
+//            bytes of dims) in fp32.
+//   The waves' states are merged through LDS in a fixed order.  A source
+//   whose valid keys fit in one chunk is finished there.  Otherwise each
+//   chunk stores its partial (max, sum, unnormalised output) in the
+//   workspace and exits without waiting.
+//   One merger workgroup per (b, h), placed after all chunk workgroups in
+//   the grid (so dispatched after them), reads the chunks' records, merges
+//   them in chunk order, normalises and writes the output.  Each record word
+//   carries a tag of the call, so the merger knows when a record is
+//   complete; no fence, counter or clearing of the workspace is needed.
 // Rows j >= src_len[b] are never read.  The chunk size depends only on the
 // row size, and each beam's arithmetic is the same whatever k is, so the
 // output bits do not depend on k, B or the beam's position.
 #include <math.h>
+
+#include <algorithm>
 
 #include "launch.h"
 
@@ -36,15 +44,36 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kWaves = 4;
 constexpr int kBlock = kWave * kWaves;
-constexpr int kTile = kWave;  // keys per wave tile: one key per lane
+constexpr int kIt = 8;   // row loads of K (and of V) per lane per tile
+constexpr int kXcds = 8; // MI355X: workgroups go round-robin to 8 XCDs
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 template <bool BF16>
 struct Elem {
     static constexpr int size = BF16 ? 2 : 4;
     static constexpr int per16 = 16 / size;  // elements in 16 bytes
 };
+
+template <int D, bool BF16>
+struct Geo {
+    static constexpr int kEpl = Elem<BF16>::per16;   // elements per lane slice
+    static constexpr int kLpr = D / kEpl;            // lanes sharing one row
+    static constexpr int kRpi = kWave / kLpr;        // rows per wave instruction
+    static constexpr int kTile = kIt * kRpi;         // keys per wave tile
+    static constexpr int kChunk = kWaves * kTile;    // keys per workgroup
+    static constexpr int kDup = kLpr > 8 ? kLpr / 8 : 1;   // lanes sharing a score row
+    static constexpr int kRows = kLpr < 8 ? 8 / kLpr : 1;  // score rows per lane
+    static constexpr int kPStride = kTile + kTile / 8;     // LDS rows per wave (padded)
+    static_assert(kLpr >= 2 && kLpr <= 32, "row must be 32..512 bytes");
+    static_assert(kIt == 8, "the reduce-scatter assumes 8 row loads per lane");
+};
+
+__device__ __forceinline__ uint4 load_nt(const uint4 *p) {
+    const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -85,60 +114,124 @@ __device__ __forceinline__ void unpack16(uint4 a, float *f) {
     }
 }
 
-// Cross-lane moves.  DPP quad_perm/row mirrors stay inside a row of 16
-// lanes; ds_swizzle covers the 32-lane halves and ds_bpermute the rest.
+// ---- cross-lane exchange ---------------------------------------------------
+// DPP stays inside a row of 16 lanes, ds_swizzle inside 32 lanes, and
+// ds_bpermute covers the whole wave.
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
         0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
 }
-constexpr int kQuadXor1 = 0xB1;        // quad_perm [1,0,3,2]
-constexpr int kQuadXor2 = 0x4E;        // quad_perm [2,3,0,1]
-constexpr int kRowHalfMirror = 0x141;  // lane i <-> 7-i within 8 lanes
-constexpr int kRowMirror = 0x140;      // lane i <-> 15-i within 16 lanes
-
-__device__ __forceinline__ float swz_xor16(float x) {
-    // BitMode swizzle inside 32 lanes: and 0x1f, or 0, xor 0x10.
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+template <int PATTERN>
+__device__ __forceinline__ float swizzle(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), PATTERN));
 }
-
-__device__ __forceinline__ float shfl_xor(float x, int mask);
-
-// Butterfly all-reduce over the 64 lanes; every lane gets the same value.
-// Each step combines (own, partner) with a commutative operation, so the
-// two lanes of a pair compute bit-identical results.
-__device__ __forceinline__ float wave_max(float x) {
-    x = fmaxf(x, dpp<kQuadXor1>(x));
-    x = fmaxf(x, dpp<kQuadXor2>(x));
-    x = fmaxf(x, dpp<kRowHalfMirror>(x));
-    x = fmaxf(x, dpp<kRowMirror>(x));
-    x = fmaxf(x, swz_xor16(x));
-    x = fmaxf(x, shfl_xor(x, 32));
-    return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-    x += dpp<kQuadXor1>(x);
-    x += dpp<kQuadXor2>(x);
-    x += dpp<kRowHalfMirror>(x);
-    x += dpp<kRowMirror>(x);
-    x += swz_xor16(x);
-    x += shfl_xor(x, 32);
-    return x;
-}
-
-__device__ __forceinline__ float shfl_xor(float x, int mask) {
-    const int lane = __lane_id();
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((lane ^ mask) << 2,
+__device__ __forceinline__ float lane_xor(float x, int mask) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((__lane_id() ^ mask) << 2,
                                                                   __builtin_bit_cast(int, x)));
 }
 
-// Sum over the lanes that share (lane % Group): the lane groups of the PV
-// layout hold partial sums of the same dims for different rows.
-template <int Group>
-__device__ __forceinline__ float sum_across_groups(float x) {
-#pragma unroll
-    for (int mask = Group; mask < kWave; mask <<= 1) x += shfl_xor(x, mask);
+// Value of lane (lane ^ MASK), for MASK a power of two below 64.
+template <int MASK>
+__device__ __forceinline__ float xor_lane(float x) {
+    if constexpr (MASK == 1) return dpp<0xB1>(x);              // quad_perm [1,0,3,2]
+    else if constexpr (MASK == 2) return dpp<0x4E>(x);         // quad_perm [2,3,0,1]
+    else if constexpr (MASK == 8) return dpp<0x128>(x);        // row_ror:8 == xor 8 in a row
+    else if constexpr (MASK < 32) return swizzle<0x1F | (MASK << 10)>(x);  // bit mode, xor MASK
+    else return lane_xor(x, MASK);
+}
+
+// Sum over the kLpr lanes of a row group (every lane of the group gets the
+// bit-identical result: each step pairs lanes and adds commutatively).
+template <int G>
+__device__ __forceinline__ float group_sum(float x) {
+    if constexpr (G >= 2) x += dpp<0xB1>(x);
+    if constexpr (G >= 4) x += dpp<0x4E>(x);
+    if constexpr (G >= 8) x += dpp<0x141>(x);   // row_half_mirror: other quad of the 8
+    if constexpr (G >= 16) x += dpp<0x140>(x);  // row_mirror: other 8 of the 16
+    if constexpr (G >= 32) x += swizzle<0x401F>(x);
     return x;
+}
+
+// Reduction over the row groups of a wave (lanes sharing lane % G).
+template <int G, int MASK = G>
+__device__ __forceinline__ float groups_max(float x) {
+    if constexpr (MASK < kWave) {
+        x = fmaxf(x, xor_lane<MASK>(x));
+        return groups_max<G, MASK * 2>(x);
+    } else {
+        return x;
+    }
+}
+template <int G, int MASK = G>
+__device__ __forceinline__ float groups_sum(float x) {
+    if constexpr (MASK < kWave) {
+        x += xor_lane<MASK>(x);
+        return groups_sum<G, MASK * 2>(x);
+    } else {
+        return x;
+    }
+}
+
+// All-reduce over the 64 lanes (every lane gets the bit-identical result).
+__device__ __forceinline__ float wave_max(float x) {
+    x = fmaxf(x, dpp<0xB1>(x));
+    x = fmaxf(x, dpp<0x4E>(x));
+    x = fmaxf(x, dpp<0x141>(x));
+    x = fmaxf(x, dpp<0x140>(x));
+    x = fmaxf(x, swizzle<0x401F>(x));
+    x = fmaxf(x, lane_xor(x, 32));
+    return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+    x += dpp<0xB1>(x);
+    x += dpp<0x4E>(x);
+    x += dpp<0x141>(x);
+    x += dpp<0x140>(x);
+    x += swizzle<0x401F>(x);
+    x += lane_xor(x, 32);
+    return x;
+}
+
+// Partner value for step MASK of a butterfly inside a row group of G lanes.
+// The first step (MASK == G/2) may pair lane s with G-1-s (a mirror, which
+// DPP does cheaply); later steps must pair s with s ^ MASK exactly.
+template <int G, int MASK>
+__device__ __forceinline__ float group_partner(float x) {
+    if constexpr (MASK == G / 2 && MASK == 4) return dpp<0x141>(x);   // row_half_mirror
+    else if constexpr (MASK == G / 2 && MASK == 8) return dpp<0x140>(x);  // row_mirror
+    else return xor_lane<MASK>(x);
+}
+
+// Reduce-scatter of the QK^T partial sums inside a row group of G lanes.
+// On entry every lane holds, for the tile's 8 row loads u and each beam i,
+// its own 16-byte slice of the dot product d[u][i].  On exit d[j][i],
+// j < max(1, 8/G), holds the complete dot product of row
+// u = (sub / max(1, G/8)) * max(1, 8/G) + j: the 8*KB sums are spread over
+// the group instead of being repeated in every lane, so each score is
+// turned into a probability once (G/8 times when G > 8).
+template <int G, int KB, int MASK = G / 2, int NR = 8>
+__device__ __forceinline__ void group_reduce_scatter(float (&d)[8][KB], int sub) {
+    if constexpr (MASK >= 1) {
+        if constexpr (NR > 1) {
+            constexpr int HALF = NR / 2;
+            const bool up = (sub & MASK) != 0;
+#pragma unroll
+            for (int j = 0; j < HALF; ++j) {
+#pragma unroll
+                for (int i = 0; i < KB; ++i) {
+                    const float send = up ? d[j][i] : d[j + HALF][i];
+                    const float keep = up ? d[j + HALF][i] : d[j][i];
+                    d[j][i] = keep + group_partner<G, MASK>(send);
+                }
+            }
+            group_reduce_scatter<G, KB, MASK / 2, HALF>(d, sub);
+        } else {
+#pragma unroll
+            for (int i = 0; i < KB; ++i) d[0][i] += group_partner<G, MASK>(d[0][i]);
+            group_reduce_scatter<G, KB, MASK / 2, 1>(d, sub);
+        }
+    }
 }
 
 // Merge softmax state (mb, lb, ab) into (m, l, a); m in the base-2 domain.
@@ -152,59 +245,147 @@ __device__ __forceinline__ void merge_state(float &m, float &l, float &a, float 
     m = mx;
 }
 
-template <int D, bool BF16, int KB>
-struct Cfg {
-    static constexpr int kEpl = Elem<BF16>::per16;  // elements per 16-byte slice
-    static constexpr int kSlices = D / kEpl;        // 16-byte slices per row
-    static constexpr int kLpr = kSlices;            // PV: lanes sharing one V row
-    static constexpr int kRpi = kWave / kLpr;       // PV: rows per wave instruction
-    static_assert(kSlices >= 2 && kSlices <= 32, "row must be 32..512 bytes");
-};
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
 
-// Kernel 1: one workgroup per (b, h, chunk).  Chunk c covers keys
-// [c*C, c*C + C) with C = kWaves * kTile * tiles_per_wave.
+template <bool BF16>
+__device__ __forceinline__ void store_out(void *out, size_t idx, float v) {
+    if constexpr (BF16)
+        static_cast<uint16_t *>(out)[idx] = f32_to_bf16_rne(v);
+    else
+        static_cast<float *>(out)[idx] = v;
+}
+
+// Bound on re-reads of a partial-record word that does not yet carry the
+// current call's tag (about 10 ms at most; not reached in practice).
+constexpr int kMaxSpins = 1 << 14;
+
+// Merger for (b, h) = bh: merges the chunk records of a source with more
+// than one chunk, in chunk order, and writes the normalised output.
+//
+// Each record word is (call tag << 32 | fp32 bits), written and read with
+// device-scope atomics: every word is coherent across XCDs by itself, and
+// the tag tells whether it was written by this call, so no fence or counter
+// is needed.  The chunk workgroups have lower ids and were dispatched
+// earlier, and they wait on nothing, so their records arrive; a word that
+// does not carry this call's tag yet is re-read a bounded number of times,
+// and the output becomes NaN if it never does (a loud failure instead of a
+// silent wrong merge or an endless wait).
 template <int D, bool BF16, int KB>
-__global__ __launch_bounds__(kBlock) void cross_attn_chunks(
-    const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
-    const int32_t *__restrict__ src_len, float *__restrict__ part,
-    int H, int S, int C, int NC, float scale_log2)
+__device__ __forceinline__ void merge_chunks(const unsigned long long *__restrict__ part,
+                                             const int32_t *__restrict__ src_len, void *__restrict__ out,
+                                             int bh, int n_bh, int H, int S, int NC,
+                                             unsigned long long epoch)
 {
-    using CF = Cfg<D, BF16, KB>;
-    constexpr int kS = CF::kSlices;
-    constexpr int kEpl = CF::kEpl;
-    constexpr int kLpr = CF::kLpr;
-    constexpr int kRpi = CF::kRpi;
-
-    __shared__ uint4 q_lds[KB * kS];
-    __shared__ float p_lds[kWaves][kTile][KB];
-    __shared__ float m_lds[kWaves][KB], l_lds[kWaves][KB];
-    __shared__ float a_lds[kWaves][KB][D];
-
-    const int bh = blockIdx.x / NC;
-    const int c = blockIdx.x - bh * NC;
+    using G = Geo<D, BF16>;
+    if (bh >= n_bh) return;
     const int b = bh / H;
     const int h = bh - b * H;
     const int L = min(max(src_len[b], 0), S);
-    const int j0 = c * C;
-    if (j0 >= L) return;  // whole chunk is padding: never read
-    const int j1 = min(j0 + C, L);
+    const int nc = (L + G::kChunk - 1) / G::kChunk;
+    if (nc <= 1) return;  // written by the chunk workgroup itself
+    constexpr int kRec = KB * (D + 2);
+    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
+    const unsigned long long *recs = part + (size_t)bh * NC * kRec;
+    const size_t obase = ((size_t)b * KB * H + h) * D;
+    constexpr int kBatch = 4;  // chunks whose words are loaded together
+    for (int x = threadIdx.x; x < KB * D; x += kBlock) {
+        const int i = x / D, d = x - i * D;
+        const int at[3] = {KB * D + i, KB * D + KB + i, x};  // m, l, acc
+        float mm = -INFINITY, ll = 0.f, aa = 0.f;
+        bool stale = false;
+        for (int c0 = 0; c0 < nc; c0 += kBatch) {
+            unsigned long long wv[kBatch][3];
+#pragma unroll
+            for (int q2 = 0; q2 < kBatch; ++q2) {
+#pragma unroll
+                for (int f = 0; f < 3; ++f) {
+                    wv[q2][f] = tag;
+                    if (c0 + q2 < nc)
+                        wv[q2][f] = __hip_atomic_load(recs + (size_t)(c0 + q2) * kRec + at[f],
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+#pragma unroll
+            for (int q2 = 0; q2 < kBatch; ++q2) {
+                if (c0 + q2 >= nc) break;
+#pragma unroll
+                for (int f = 0; f < 3; ++f) {
+                    const unsigned long long *a = recs + (size_t)(c0 + q2) * kRec + at[f];
+                    for (int spin = 0; (wv[q2][f] & 0xffffffff00000000ull) != tag && spin < kMaxSpins; ++spin) {
+                        __builtin_amdgcn_s_sleep(2);
+                        wv[q2][f] = __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    stale |= (wv[q2][f] & 0xffffffff00000000ull) != tag;
+                }
+                merge_state(mm, ll, aa, __uint_as_float((uint32_t)wv[q2][0]),
+                            __uint_as_float((uint32_t)wv[q2][1]), __uint_as_float((uint32_t)wv[q2][2]));
+            }
+        }
+        store_out<BF16>(out, obase + (size_t)i * H * D + d, stale ? NAN : aa / ll);
+    }
+}
 
+template <int D, bool BF16, int KB>
+__global__ __launch_bounds__(kBlock) void cross_attn_kernel(
+    const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
+    const int32_t *__restrict__ src_len, void *__restrict__ out,
+    unsigned long long *__restrict__ part,
+    int n_bh, int H, int S, int NC, float scale_log2, unsigned long long epoch)
+{
+    using G = Geo<D, BF16>;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kRpi = G::kRpi;
+    constexpr int kTile = G::kTile, kChunk = G::kChunk;
+
+    __shared__ float m_lds[kWaves][KB], l_lds[kWaves][KB];
+    __shared__ float a_lds[kWaves][KB][D];
+    __shared__ __attribute__((aligned(16))) float p_lds[kWaves][G::kPStride][KB];
+
+    // Workgroup g runs on XCD g % 8 (round-robin dispatch).  All chunks of
+    // one (b, h), and its merger, get ids with the same residue, so they
+    // share an L2.  Merger workgroups come after every chunk workgroup.
+    const int g = blockIdx.x;
+    const int n_chunk_blocks = ((n_bh + kXcds - 1) / kXcds) * kXcds * NC;
+    if (g >= n_chunk_blocks) {
+        merge_chunks<D, BF16, KB>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC, epoch);
+        return;
+    }
+    const int xcd = g % kXcds;
+    const int slot = g / kXcds;
+    const int bh = (slot / NC) * kXcds + xcd;
+    const int c = slot - (slot / NC) * NC;
+    if (bh >= n_bh) return;
+    const int b = bh / H;
+    const int h = bh - b * H;
+    const int L = min(max(src_len[b], 0), S);
+    const int j0 = c * kChunk;
+    const int nc = (L + kChunk - 1) / kChunk;
     const int tid = threadIdx.x;
+    const size_t obase = ((size_t)b * KB * H + h) * D;  // out[b, 0, h, 0]
+    if (L == 0) {  // no valid key: the output row is zero
+        if (c == 0)
+            for (int x = tid; x < KB * D; x += kBlock)
+                store_out<BF16>(out, obase + (size_t)(x / D) * H * D + x % D, 0.f);
+        return;
+    }
+    if (c >= nc) return;  // chunk lies in the padding: never read
+    const int j1 = min(j0 + kChunk, L);
+
     const int lane = tid & (kWave - 1);
     const int w = tid / kWave;
+    const int sub = lane % kLpr;  // 16-byte slice of the row this lane reads
+    const int grp = lane / kLpr;  // row of the instruction this lane reads
 
-    // k queries of (b, h): q[b, i, h, :] for i < KB
-    for (int x = tid; x < KB * kS; x += kBlock) {
-        const int i = x / kS, s = x - i * kS;
-        q_lds[x] = q[((size_t)(b * KB + i) * H + h) * kS + s];
-    }
-    __syncthreads();
+    uint4 qr[KB];
+#pragma unroll
+    for (int i = 0; i < KB; ++i) qr[i] = q[((size_t)(b * KB + i) * H + h) * kLpr + sub];
 
-    const uint4 *Kbh = K + (size_t)bh * S * kS;
-    const uint4 *Vbh = V + (size_t)bh * S * kS;
-
-    const int sub = lane % kLpr;  // PV: this lane's slice of the row
-    const int grp = lane / kLpr;  // PV: this lane's row within an instruction
+    const uint4 *Kbh = K + (size_t)bh * S * kLpr;
+    const uint4 *Vbh = V + (size_t)bh * S * kLpr;
 
     float m[KB], l[KB], acc[KB][kEpl];
 #pragma unroll
@@ -215,82 +396,82 @@ __global__ __launch_bounds__(kBlock) void cross_attn_chunks(
         for (int e = 0; e < kEpl; ++e) acc[i][e] = 0.f;
     }
 
-    // Every wave runs the same number of iterations (the loop holds
-    // barriers); a wave whose tile lies past j1 sees only invalid keys.
-    for (int tb = j0; tb < j1; tb += kWaves * kTile) {
-        const int t0 = tb + w * kTile;
-        // ---- QK^T: lane owns key t0 + lane -------------------------------
-        const int j = t0 + lane;
-        const bool valid = j < j1;
-        uint4 kr[kS];
+    const int t0 = j0 + w * kTile;
+    if (t0 < j1) {
+        // Row loads: instruction u reads rows t0 + u*kRpi + grp.  Rows past
+        // j1 re-read row j1 - 1 (valid data, never padding) and are masked.
+        uint4 kr[kIt], vr[kIt];
 #pragma unroll
-        for (int s = 0; s < kS; ++s) kr[s] = make_uint4(0, 0, 0, 0);
-        if (valid) {
-#pragma unroll
-            for (int s = 0; s < kS; ++s) kr[s] = Kbh[(size_t)j * kS + s];
+        for (int u = 0; u < kIt; ++u) {
+            const int j = min(t0 + u * kRpi + grp, j1 - 1);
+            kr[u] = load_nt(Kbh + (size_t)j * kLpr + sub);
+            vr[u] = load_nt(Vbh + (size_t)j * kLpr + sub);
         }
-        // V slices for the PV layout: instruction u covers rows u*kRpi + grp
-        uint4 vr[kTile / kRpi];
+        // QK^T: partial dots of this lane's slice, then a reduce-scatter in
+        // the row group, after which the lane owns whole score rows.
+        float d[kIt][KB];
 #pragma unroll
-        for (int u = 0; u < kTile / kRpi; ++u) {
-            const int jv = t0 + u * kRpi + grp;
-            vr[u] = make_uint4(0, 0, 0, 0);
-            if (jv < j1) vr[u] = Vbh[(size_t)jv * kS + sub];
+        for (int u = 0; u < kIt; ++u) {
+#pragma unroll
+            for (int i = 0; i < KB; ++i) d[u][i] = dot16<BF16>(qr[i], kr[u], 0.f);
         }
-
-        float s_[KB];
+        group_reduce_scatter<kLpr, KB>(d, sub);
+        constexpr int kRows = G::kRows, kDup = G::kDup;
+        const int u0 = (sub / kDup) * kRows;  // first score row of this lane
+        float mt[KB];
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
-            float d = 0.f;
+            float mx = -INFINITY;
 #pragma unroll
-            for (int s = 0; s < kS; ++s) d = dot16<BF16>(q_lds[i * kS + s], kr[s], d);
-            s_[i] = valid ? d * scale_log2 : -INFINITY;
+            for (int j = 0; j < kRows; ++j) {
+                const bool ok = t0 + (u0 + j) * kRpi + grp < j1;
+                d[j][i] = ok ? d[j][i] * scale_log2 : -INFINITY;
+                mx = fmaxf(mx, d[j][i]);
+            }
+            mt[i] = wave_max(mx);  // tile maximum (finite: key t0 is valid)
         }
-
-        // ---- softmax over the tile, once per (key, beam) -----------------
-        float p[KB];
+        float* prow = &p_lds[w][0][0];
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
-            const float mt = wave_max(s_[i]);
-            const float ms = (mt == -INFINITY) ? 0.f : mt;
-            p[i] = __builtin_amdgcn_exp2f(s_[i] - ms);
-            const float lt = wave_sum(p[i]);
-            // fold the tile into the running state (wave-uniform m, l)
-            const float mx = fmaxf(m[i], mt);
-            const float mxs = (mx == -INFINITY) ? 0.f : mx;
-            const float fo = __builtin_amdgcn_exp2f(m[i] - mxs);  // old state
-            const float fn = __builtin_amdgcn_exp2f(mt - mxs);    // this tile
-            l[i] = l[i] * fo + lt * fn;
+            float lsum = 0.f;
 #pragma unroll
-            for (int e = 0; e < kEpl; ++e) acc[i][e] *= fo;
-            m[i] = mx;
-            p[i] *= fn;
+            for (int j = 0; j < kRows; ++j) {
+                d[j][i] = __builtin_amdgcn_exp2f(d[j][i] - mt[i]);
+                lsum += d[j][i];
+            }
+            l[i] = wave_sum(sub % kDup == 0 ? lsum : 0.f);
+            m[i] = mt[i];
         }
 #pragma unroll
-        for (int i = 0; i < KB; ++i) p_lds[w][lane][i] = p[i];
-        __syncthreads();
-
-        // ---- PV: coalesced rows, weights broadcast from LDS ---------------
+        for (int j = 0; j < kRows; ++j) {
+            const int r = (u0 + j) * kRpi + grp;
 #pragma unroll
-        for (int u = 0; u < kTile / kRpi; ++u) {
+            for (int i = 0; i < KB; ++i) prow[(r + (r >> 3)) * KB + i] = d[j][i];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // PV: the coalesced V rows with their weights read back from LDS
+#pragma unroll
+        for (int u = 0; u < kIt; ++u) {
             const int r = u * kRpi + grp;
+            float pw[KB];
+#pragma unroll
+            for (int i = 0; i < KB; ++i) pw[i] = prow[(r + (r >> 3)) * KB + i];
             float vf[kEpl];
             unpack16<BF16>(vr[u], vf);
 #pragma unroll
             for (int i = 0; i < KB; ++i) {
-                const float pw = p_lds[w][r][i];
 #pragma unroll
-                for (int e = 0; e < kEpl; ++e) acc[i][e] = fmaf(pw, vf[e], acc[i][e]);
+                for (int e = 0; e < kEpl; ++e) acc[i][e] = fmaf(pw[i], vf[e], acc[i][e]);
             }
         }
-        __syncthreads();
-    }
-
-    // ---- merge: lane groups of the wave (same m, l), then the 4 waves ----
+        // the row groups hold partial sums of the same dims for different rows
 #pragma unroll
-    for (int i = 0; i < KB; ++i) {
+        for (int i = 0; i < KB; ++i) {
 #pragma unroll
-        for (int e = 0; e < kEpl; ++e) acc[i][e] = sum_across_groups<kLpr>(acc[i][e]);
+            for (int e = 0; e < kEpl; ++e) acc[i][e] = groups_sum<kLpr>(acc[i][e]);
+        }
     }
     if (lane < kLpr) {
 #pragma unroll
@@ -308,88 +489,70 @@ __global__ __launch_bounds__(kBlock) void cross_attn_chunks(
     }
     __syncthreads();
 
-    // partial record of (b, h, c): acc[KB][D], then m[KB], then l[KB]
-    float *rec = part + ((size_t)bh * NC + c) * (size_t)(KB * (D + 2));
+    if (nc == 1) {
+        for (int x = tid; x < KB * D; x += kBlock) {
+            const int i = x / D, d = x - i * D;
+            float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds[0][i][d];
+#pragma unroll
+            for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds[ww][i][d]);
+            store_out<BF16>(out, obase + (size_t)i * H * D + d, aa / ll);
+        }
+        return;
+    }
+
+    // Partial record of (b, h, c): acc[KB][D], then m[KB], then l[KB].
+    unsigned long long *rec = part + ((size_t)bh * NC + c) * (KB * (D + 2));
+    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     for (int x = tid; x < KB * D; x += kBlock) {
         const int i = x / D, d = x - i * D;
         float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds[0][i][d];
 #pragma unroll
         for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds[ww][i][d]);
-        rec[x] = aa;
+        __hip_atomic_store(rec + x, tag | __float_as_uint(aa), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (d == 0) {
-            rec[KB * D + i] = mm;
-            rec[KB * D + KB + i] = ll;
+            __hip_atomic_store(rec + KB * D + i, tag | __float_as_uint(mm), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(rec + KB * D + KB + i, tag | __float_as_uint(ll), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
         }
-    }
-}
-
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
-// Kernel 2: one workgroup per (b, h); thread x = (beam i, dim d).
-template <bool BF16, int KB>
-__global__ __launch_bounds__(kBlock) void cross_attn_combine(
-    const float *__restrict__ part, const int32_t *__restrict__ src_len, void *__restrict__ out,
-    int H, int S, int D, int C, int NC)
-{
-    const int bh = blockIdx.x;
-    const int b = bh / H;
-    const int h = bh - b * H;
-    const int L = min(max(src_len[b], 0), S);
-    const int nc = (L + C - 1) / C;
-    const size_t rs = (size_t)KB * (D + 2);
-    for (int x = threadIdx.x; x < KB * D; x += blockDim.x) {
-        const int i = x / D, d = x - i * D;
-        float m = -INFINITY, l = 0.f, a = 0.f;
-        for (int c = 0; c < nc; ++c) {
-            const float *rec = part + ((size_t)bh * NC + c) * rs;
-            merge_state(m, l, a, rec[KB * D + i], rec[KB * D + KB + i], rec[x]);
-        }
-        const float o = (nc == 0) ? 0.f : a / l;
-        const size_t oi = ((size_t)(b * KB + i) * H + h) * D + d;
-        if constexpr (BF16)
-            static_cast<uint16_t *>(out)[oi] = f32_to_bf16_rne(o);
-        else
-            static_cast<float *>(out)[oi] = o;
     }
 }
 
 template <int D, bool BF16, int KB>
 hipError_t launch_typed(const void *q, const void *K, const void *V, const int32_t *src_len,
-                        void *out, int B, int H, int S, float *ws, hipStream_t stream)
+                        void *out, int B, int H, int S, float *ws, unsigned long long epoch,
+                        hipStream_t stream)
 {
-    const int C = cross_attn_chunk_keys(D, Elem<BF16>::size);
-    const int NC = (S + C - 1) / C;
+    using G = Geo<D, BF16>;
+    // at least one chunk column, so that a source with no valid key (or
+    // S == 0) still has a workgroup to write its zero output
+    const int NC = max(1, (S + G::kChunk - 1) / G::kChunk);
+    const int n_bh = B * H;
     const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
-    const long long nblk = (long long)B * H * NC;
-    if (nblk > 0) {
-        hipLaunchKernelGGL((cross_attn_chunks<D, BF16, KB>), dim3((unsigned)nblk), dim3(kBlock), 0,
-                           stream, static_cast<const uint4 *>(q), static_cast<const uint4 *>(K),
-                           static_cast<const uint4 *>(V), src_len, ws, H, S, C, NC,
-                           (float)scale_log2);
-    }
-    hipLaunchKernelGGL((cross_attn_combine<BF16, KB>), dim3((unsigned)(B * H)), dim3(kBlock), 0,
-                       stream, ws, src_len, out, H, S, D, C, NC);
+    unsigned long long *part = reinterpret_cast<unsigned long long *>(ws);
+    const long long groups = ((long long)n_bh + kXcds - 1) / kXcds;
+    const long long nblk = groups * kXcds * NC + (NC > 1 ? n_bh : 0);  // chunks, then mergers
+    hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB>), dim3((unsigned)nblk), dim3(kBlock), 0,
+                       stream, static_cast<const uint4 *>(q), static_cast<const uint4 *>(K),
+                       static_cast<const uint4 *>(V), src_len, out, part, n_bh, H, S,
+                       NC, (float)scale_log2, epoch);
     return hipGetLastError();
 }
 
 template <int D, bool BF16>
 hipError_t launch_k(int k, const void *q, const void *K, const void *V, const int32_t *src_len,
-                    void *out, int B, int H, int S, float *ws, hipStream_t stream)
+                    void *out, int B, int H, int S, float *ws, unsigned long long epoch,
+                    hipStream_t stream)
 {
     switch (k) {
-    case 1: return launch_typed<D, BF16, 1>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 2: return launch_typed<D, BF16, 2>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 3: return launch_typed<D, BF16, 3>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 4: return launch_typed<D, BF16, 4>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 5: return launch_typed<D, BF16, 5>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 6: return launch_typed<D, BF16, 6>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 7: return launch_typed<D, BF16, 7>(q, K, V, src_len, out, B, H, S, ws, stream);
-    case 8: return launch_typed<D, BF16, 8>(q, K, V, src_len, out, B, H, S, ws, stream);
+    case 1: return launch_typed<D, BF16, 1>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 2: return launch_typed<D, BF16, 2>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 3: return launch_typed<D, BF16, 3>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 4: return launch_typed<D, BF16, 4>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 5: return launch_typed<D, BF16, 5>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 6: return launch_typed<D, BF16, 6>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 7: return launch_typed<D, BF16, 7>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 8: return launch_typed<D, BF16, 8>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -397,13 +560,13 @@ hipError_t launch_k(int k, const void *q, const void *K, const void *V, const in
 template <bool BF16>
 hipError_t launch_d(int D, int k, const void *q, const void *K, const void *V,
                     const int32_t *src_len, void *out, int B, int H, int S, float *ws,
-                    hipStream_t stream)
+                    unsigned long long epoch, hipStream_t stream)
 {
     switch (D) {
-    case 16: return launch_k<16, BF16>(k, q, K, V, src_len, out, B, H, S, ws, stream);
-    case 32: return launch_k<32, BF16>(k, q, K, V, src_len, out, B, H, S, ws, stream);
-    case 64: return launch_k<64, BF16>(k, q, K, V, src_len, out, B, H, S, ws, stream);
-    case 128: return launch_k<128, BF16>(k, q, K, V, src_len, out, B, H, S, ws, stream);
+    case 16: return launch_k<16, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 32: return launch_k<32, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 64: return launch_k<64, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    case 128: return launch_k<128, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -411,23 +574,25 @@ hipError_t launch_d(int D, int k, const void *q, const void *K, const void *V,
 }  // namespace
 
 int cross_attn_chunk_keys(int D, int esize) {
-    (void)D;
-    (void)esize;
-    return kWaves * kTile;  // one 64-key tile per wave
+    // kWaves * kIt rows of 64/(lanes per row) = 4 * 8 * 64 * 16 / (D * esize)
+    return kWaves * kIt * kWave * 16 / (D * esize);
 }
 
 size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize) {
     const int C = cross_attn_chunk_keys(D, esize);
-    const size_t NC = (size_t)((S + C - 1) / C);
-    return (size_t)B * H * NC * (size_t)k * (size_t)(D + 2);
+    const size_t NC = (size_t)std::max(1, (S + C - 1) / C);
+    const size_t n_bh = (size_t)B * H;
+    const size_t part = n_bh * NC * (size_t)k * (size_t)(D + 2);
+    // 64-bit partial-record words
+    return 2 * part;
 }
 
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len,
                              void *out, int B, int k, int H, int S, int D, bool bf16,
-                             float *workspace, hipStream_t stream)
+                             float *workspace, unsigned long long epoch, hipStream_t stream)
 {
-    return bf16 ? launch_d<true>(D, k, q, K, V, src_len, out, B, H, S, workspace, stream)
-                : launch_d<false>(D, k, q, K, V, src_len, out, B, H, S, workspace, stream);
+    return bf16 ? launch_d<true>(D, k, q, K, V, src_len, out, B, H, S, workspace, epoch, stream)
+                : launch_d<false>(D, k, q, K, V, src_len, out, B, H, S, workspace, epoch, stream);
 }
 
 }  // namespace fs

@@ -15,13 +15,16 @@ namespace fs {
 // source is read by one beam or by k beams.
 int cross_attn_chunk_keys(int D, int esize);
 
-// Number of fp32 values the per-chunk partials take for these sizes.
+// Workspace size in 4-byte words: the per-chunk partial records.
 size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize);
 
+// `epoch` must differ from the epoch of every earlier call that used the
+// same workspace: its low 32 bits tag the partial records, which are never
+// cleared.
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
                              const int32_t *src_len, void *out,
                              int B, int k, int H, int S, int D, bool bf16,
-                             float *workspace, hipStream_t stream);
+                             float *workspace, unsigned long long epoch, hipStream_t stream);
 
 hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t,
                               int n, float *logits, int V, hipStream_t stream);

@@ -150,3 +150,21 @@ def test_caller_buffers_and_workspace_reuse():
     with pytest.raises(Exception):
         api.beam_cross_attn(to_dev(d["q"]), to_dev(d["K"]), to_dev(d["V"]),
                             to_dev(d["src_len"]), workspace=ws[:16])
+
+
+def test_workspace_reused_across_calls_with_changing_lengths():
+    # The completion counters in the workspace are never cleared; each call
+    # must still find its own last chunk.  Reuse one workspace for calls whose
+    # chunk counts differ, then for a different problem size.
+    dev = device()
+    rng = np.random.default_rng(51)
+    need = api.beam_cross_attn_workspace_bytes(6, 4, 3, 1100, 64, torch.bfloat16)
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=dev)
+    for rep in range(6):
+        lens = rng.integers(0, 1101, size=6)
+        lens[rep % 6] = 1100
+        d = random_case(6, 4, 3, 1100, 64, "bf16", lens, seed=60 + rep)
+        say(f"[attn workspace reuse] rep={rep} lens={lens.tolist()}")
+        assert_attn_close(run(d, ws=ws), oracle_attn(d), f"rep {rep}")
+    d = random_case(2, 4, 3, 300, 64, "bf16", [300, 257], seed=70)
+    assert_attn_close(run(d, ws=ws), oracle_attn(d), "smaller problem, same workspace")
