@@ -63,11 +63,11 @@ struct Geo {
     static constexpr int kRpi = kWave / kLpr;        // rows per wave instruction
     static constexpr int kTile = kIt * kRpi;         // keys per wave tile
     static constexpr int kChunk = kWaves * kTile;    // keys per workgroup
-    static constexpr int kDup = kLpr > 8 ? kLpr / 8 : 1;   // lanes sharing a score row
-    static constexpr int kRows = kLpr < 8 ? 8 / kLpr : 1;  // score rows per lane
+    static constexpr int kDup = kLpr > kIt ? kLpr / kIt : 1;   // lanes sharing a score row
+    static constexpr int kRows = kLpr < kIt ? kIt / kLpr : 1;  // score rows per lane
     static constexpr int kPStride = kTile + kTile / 8;     // LDS rows per wave (padded)
     static_assert(kLpr >= 2 && kLpr <= 32, "row must be 32..512 bytes");
-    static_assert(kIt == 8, "the reduce-scatter assumes 8 row loads per lane");
+    static_assert(kIt == 8 || kIt == 16, "the row-load count must be a power of two >= 8");
 };
 
 __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
@@ -204,14 +204,14 @@ __device__ __forceinline__ float group_partner(float x) {
 }
 
 // Reduce-scatter of the QK^T partial sums inside a row group of G lanes.
-// On entry every lane holds, for the tile's 8 row loads u and each beam i,
+// On entry every lane holds, for the tile's NI row loads u and each beam i,
 // its own 16-byte slice of the dot product d[u][i].  On exit d[j][i],
-// j < max(1, 8/G), holds the complete dot product of row
-// u = (sub / max(1, G/8)) * max(1, 8/G) + j: the 8*KB sums are spread over
-// the group instead of being repeated in every lane, so each score is
-// turned into a probability once (G/8 times when G > 8).
-template <int G, int KB, int MASK = G / 2, int NR = 8>
-__device__ __forceinline__ void group_reduce_scatter(float (&d)[8][KB], int sub) {
+// j < max(1, NI/G), holds the complete dot product of row
+// u = (sub / max(1, G/NI)) * max(1, NI/G) + j: the NI*KB sums are spread
+// over the group instead of being repeated in every lane, so each score is
+// turned into a probability once (G/NI times when G > NI).
+template <int G, int KB, int NI, int MASK = G / 2, int NR = NI>
+__device__ __forceinline__ void group_reduce_scatter(float (&d)[NI][KB], int sub) {
     if constexpr (MASK >= 1) {
         if constexpr (NR > 1) {
             constexpr int HALF = NR / 2;
@@ -225,11 +225,11 @@ __device__ __forceinline__ void group_reduce_scatter(float (&d)[8][KB], int sub)
                     d[j][i] = keep + group_partner<G, MASK>(send);
                 }
             }
-            group_reduce_scatter<G, KB, MASK / 2, HALF>(d, sub);
+            group_reduce_scatter<G, KB, NI, MASK / 2, HALF>(d, sub);
         } else {
 #pragma unroll
             for (int i = 0; i < KB; ++i) d[0][i] += group_partner<G, MASK>(d[0][i]);
-            group_reduce_scatter<G, KB, MASK / 2, 1>(d, sub);
+            group_reduce_scatter<G, KB, NI, MASK / 2, 1>(d, sub);
         }
     }
 }
@@ -415,7 +415,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
 #pragma unroll
             for (int i = 0; i < KB; ++i) d[u][i] = dot16<BF16>(qr[i], kr[u], 0.f);
         }
-        group_reduce_scatter<kLpr, KB>(d, sub);
+        group_reduce_scatter<kLpr, KB, kIt>(d, sub);
         constexpr int kRows = G::kRows, kDup = G::kDup;
         const int u0 = (sub / kDup) * kRows;  // first score row of this lane
         float mt[KB];
