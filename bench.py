@@ -10,10 +10,12 @@ least 1 GiB of sets so that the 256 MB last-level cache cannot hold them.
 
 Prints ONE JSON line:
   value        algorithmic bytes of the step / step time (GB/s)
-  ms_per_step  mean step time over the timed steps (events around the region)
-  roofline     the cross-attention kernel's algorithmic GB/s against 8 TB/s,
-               from HIP events recorded around every launch in the timed
-               region (on the stream the kernels run on)
+  ms_per_step  mean step time over exactly K timed steps (HIP events at the
+               two ends of the region, on the stream the kernels run on)
+  roofline     the cross-attention kernel's algorithmic GB/s against 8 TB/s:
+               its bytes per launch / its average launch duration, timed
+               with HIP events around K back-to-back launches on the same
+               stream (per-launch event records would add several us each)
   cpu_baseline the CPU oracle on the host cores, on the same inputs
 """
 from __future__ import annotations
@@ -68,6 +70,25 @@ def ngram_bytes(rows: int, t: int, bans: int) -> int:
     """Algorithmic bytes of one n-gram call: the token history is read once;
     each banned logit is one 4-byte store (the logits are never read)."""
     return rows * t * 4 + 4 * bans
+
+
+def copy_bandwidth(dev, gib: float = 1.0, reps: int = 5) -> float:
+    """Read+write GB/s of a plain 1 GiB device copy: the achievable-bandwidth reference."""
+    import torch
+    n = int(gib * (1 << 30)) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    gbps = 2 * n * 4 * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return gbps
 
 
 def copy_calibrate(gib: float) -> None:
@@ -145,39 +166,46 @@ def main() -> int:
     logits0 = logits_d.cpu().numpy()
     bans = int(np.isneginf(logits0).sum())
 
-    # ---- warm-up and timed region -----------------------------------------
+    # ---- warm-up and timed regions -----------------------------------------
+    # Region A times exactly K steps with events only at its two ends: event
+    # records between kernels would themselves add several microseconds per
+    # step.  Region B times K back-to-back cross-attention launches (same
+    # stream, same K/V rotation) for the kernel's own average duration; the
+    # n-gram step's cost is the difference between the two.
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     K_ = args.steps
     stream = torch.cuda.current_stream(dev)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K_)]
-    e_start = torch.cuda.Event(enable_timing=True)
-    e_end = torch.cuda.Event(enable_timing=True)
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
-    e_start.record(stream)
+    e[0].record(stream)
     for i in range(K_):
-        ev[i][0].record(stream)
-        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
-        ev[i][1].record(stream)
-        api.ngram_block(tokens_d, cfg.n, logits_d)
-        ev[i][2].record(stream)
-    e_end.record(stream)
+        step(i)
+    e[1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
-    region_ms = e_start.elapsed_time(e_end)
-    ca_us = np.array([ev[i][0].elapsed_time(ev[i][1]) * 1e3 for i in range(K_)])
-    ng_us = np.array([ev[i][1].elapsed_time(ev[i][2]) * 1e3 for i in range(K_)])
+    region_ms = e[0].elapsed_time(e[1])
+    e[2].record(stream)
+    for i in range(K_):
+        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
+    e[3].record(stream)
+    torch.cuda.synchronize()
+    ca_us = e[2].elapsed_time(e[3]) * 1e3 / K_
     ms_per_step = region_ms / K_
+    step_us = ms_per_step * 1e3
+    ng_us = max(step_us - ca_us, 0.0)
     b_ca = attn_bytes(cfg, lens)
     b_ng = ngram_bytes(cfg.rows, cfg.t, bans)
     b_step = b_ca + b_ng
     value = b_step / (ms_per_step * 1e-3) / 1e9
-    ca_gbps = b_ca / (ca_us.mean() * 1e-6) / 1e9
-    log(f"step {ms_per_step * 1e3:.2f} us (wall {wall / K_ * 1e6:.2f} us); cross-attn "
-        f"{ca_us.mean():.2f} us (p10 {np.percentile(ca_us, 10):.2f}, p90 {np.percentile(ca_us, 90):.2f}) "
-        f"= {ca_gbps:.0f} GB/s; n-gram {ng_us.mean():.2f} us = {100 * ng_us.mean() / (ca_us.mean() + ng_us.mean()):.1f}% of step")
+    ca_gbps = b_ca / (ca_us * 1e-6) / 1e9
+    copy_gbps = copy_bandwidth(dev)
+    log(f"step {step_us:.2f} us (wall {wall / K_ * 1e6:.2f} us) = {value:.0f} GB/s; cross-attn {ca_us:.2f} us "
+        f"= {ca_gbps:.0f} GB/s ({100 * ca_gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
+        f"{100 * ca_gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s); "
+        f"n-gram {ng_us:.2f} us = {100 * ng_us / step_us:.1f}% of the step")
 
     traffic = None
     tp = pathlib.Path(args.traffic)
@@ -206,9 +234,10 @@ def main() -> int:
         "config": {"workload": workload_name(cfg), "B": cfg.B, "k": cfg.k, "H": cfg.H, "D": cfg.D,
                    "S": cfg.S, "t": cfg.t, "V": cfg.V, "n": cfg.n, "kv_sets_rotated": R,
                    "bytes_per_step": b_step},
-        "cross_attn_us": round(float(ca_us.mean()), 3),
-        "ngram_us": round(float(ng_us.mean()), 3),
-        "ngram_share_of_step": round(float(ng_us.mean() / (ca_us.mean() + ng_us.mean())), 4),
+        "cross_attn_us": round(ca_us, 3),
+        "ngram_us": round(ng_us, 3),
+        "ngram_share_of_step": round(ng_us / step_us, 4),
+        "copy_gbps": round(copy_gbps, 1),
         "roofline": {"bound": "hbm", "kernel": "fs_beam_cross_attn", "achieved": round(ca_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ca_gbps / HBM_PEAK_GBPS, 4),
                      "algorithmic_bytes_per_launch": b_ca, "traffic": traffic},
