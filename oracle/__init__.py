@@ -9,6 +9,8 @@ module only marshals numpy arrays into it:
 
 * :func:`cross_attn` -- masked softmax(q K^T / sqrt(D)) V with one K/V copy
   per source shared by its k beams (Appendix B, Eq. 4).
+* :func:`prefix_attn` -- self-attention over a shared prefix cache plus a
+  per-beam generated-token cache, one softmax over both (Appendix A, Eq. 3).
 * :func:`ngram_block` -- no-repeat-n-gram blocking as its definition
   (Section 4.2, Algorithm 1): ban v iff (last n-1 tokens, v) already occurred.
 
@@ -39,6 +41,8 @@ def _lib():
         lib = ctypes.CDLL(str(path))
         lib.oracle_cross_attn.argtypes = [_dp, _dp, _dp, _ip, _dp] + [ctypes.c_int] * 5
         lib.oracle_cross_attn.restype = ctypes.c_int
+        lib.oracle_prefix_attn.argtypes = [_dp, _dp, _dp, _ip, _dp, _dp, ctypes.c_int, _dp] + [ctypes.c_int] * 6
+        lib.oracle_prefix_attn.restype = ctypes.c_int
         lib.oracle_ngram_block.argtypes = [_ip, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                            ctypes.c_int, _fp, ctypes.c_int]
         lib.oracle_ngram_block.restype = ctypes.c_int
@@ -101,6 +105,33 @@ def cross_attn_f64(q, K, V, src_len) -> np.ndarray:
         lens.ctypes.data_as(_ip), out.ctypes.data_as(_dp), B, k, H, S, D)
     if rc != 0:
         raise ValueError("oracle_cross_attn rejected its arguments")
+    return out
+
+
+def prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, t: int) -> np.ndarray:
+    """fp64 self-attention over a split cache (Eq. 2-3).
+
+    q [B,k,H,D]; Kp, Vp [B,H,N,D] shared prefix; prefix_len [B] int32;
+    Kt, Vt [B*k,H,T,D] per-beam generated tokens of which the first t rows
+    are used.  Inputs may be fp32, fp64 or bf16 bits (uint16).  Returns
+    out [B,k,H,D] fp64.
+    """
+    qd, Kpd, Vpd, Ktd, Vtd = (np.ascontiguousarray(widen(a)) for a in (q, Kp, Vp, Kt, Vt))
+    if qd.ndim != 4 or Kpd.ndim != 4 or Vpd.shape != Kpd.shape or Ktd.ndim != 4 or Vtd.shape != Ktd.shape:
+        raise ValueError("q [B,k,H,D], Kp/Vp [B,H,N,D], Kt/Vt [B*k,H,T,D]")
+    B, k, H, D = qd.shape
+    N, T = Kpd.shape[2], Ktd.shape[2]
+    if Kpd.shape != (B, H, N, D) or Ktd.shape != (B * k, H, T, D):
+        raise ValueError(f"shape mismatch q{qd.shape} Kp{Kpd.shape} Kt{Ktd.shape}")
+    lens = np.ascontiguousarray(np.asarray(prefix_len, dtype=np.int32))
+    if lens.shape != (B,):
+        raise ValueError("prefix_len must be [B]")
+    out = np.empty((B, k, H, D), dtype=np.float64)
+    rc = _lib().oracle_prefix_attn(qd.ctypes.data_as(_dp), Kpd.ctypes.data_as(_dp), Vpd.ctypes.data_as(_dp),
+                                   lens.ctypes.data_as(_ip), Ktd.ctypes.data_as(_dp), Vtd.ctypes.data_as(_dp),
+                                   int(t), out.ctypes.data_as(_dp), B, k, H, N, T, D)
+    if rc != 0:
+        raise ValueError("oracle_prefix_attn rejected its arguments")
     return out
 
 

@@ -14,6 +14,8 @@
  *
  *   oracle_cross_attn   encoder-decoder attention over a de-duplicated K/V
  *                       cache (Appendix B, Eq. 4), with a key-length mask.
+ *   oracle_prefix_attn  self-attention with a shared prefix cache and a per-beam
+ *                       generated-token cache (Appendix A, Eq. 2 and Eq. 3).
  *   oracle_ngram_block  no-repeat-n-gram blocking (Section 4.2, Algorithm 1)
  *                       written as its plain definition.
  */
@@ -106,6 +108,107 @@ int oracle_cross_attn(const double *q, const double *K, const double *V,
             for (int j = 0; j < L; ++j)
                 acc += w[j] * Vbh[(size_t)j * D + d];
             orow[d] = acc / Z;
+        }
+        free(w);
+    }
+    return 0;
+}
+
+/*
+ * Self-attention over a split cache (Appendix A, Eq. 2 and Eq. 3).
+ *
+ * The prefix X of a sample (prompt or source, length N) is the same for all
+ * its M beams, so its keys/values Cache_K', Cache_V' are kept once per
+ * sample, [B, 1, N, D]; the keys/values of the t generated tokens, K_t and
+ * V_t, differ per beam, [B*M, t, D].  Eq. 3 scores the query against both
+ * parts, concatenates the scores, takes one softmax over the N + t entries,
+ * splits the probabilities again and adds the two weighted sums.  Written
+ * per head, with the steps in that order.
+ *
+ * Layouts (row-major, contiguous):
+ *   q          [B, k, H, D]     query of beam i of sample b
+ *   Kp, Vp     [B, H, N, D]     shared prefix; rows j >= prefix_len[b] are padding
+ *   prefix_len [B]              valid prefix rows of sample b; clamped to [0, N]
+ *   Kt, Vt     [B*k, H, T, D]   per-beam generated tokens; rows j >= t unused
+ *   t          number of generated tokens of every beam (0 <= t <= T)
+ *   out        [B, k, H, D]
+ * Readings: the scale 1/sqrt(D) multiplies the scores; the softmax subtracts
+ * the maximum; with no key at all (prefix_len 0 and t 0) the output is 0.
+ * Returns 0, or 1 for invalid sizes (nothing is written then).
+ */
+int oracle_prefix_attn(const double *q, const double *Kp, const double *Vp,
+                       const int32_t *prefix_len, const double *Kt, const double *Vt,
+                       int t, double *out, int B, int k, int H, int N, int T, int D)
+{
+    if (B < 0 || k < 0 || H < 0 || N < 0 || T < 0 || D < 1 || t < 0 || t > T)
+        return 1;
+    if (B == 0 || k == 0 || H == 0)
+        return 0;
+    if (!q || !prefix_len || !out || (N > 0 && (!Kp || !Vp)) || (T > 0 && (!Kt || !Vt)))
+        return 1;
+
+    const double root_d = sqrt((double)D);
+    const long rows = (long)B * k * H;
+
+#pragma omp parallel for schedule(dynamic, 4)
+    for (long r = 0; r < rows; ++r) {
+        /* r = (b*k + i)*H + h: sample b, beam i, head h; hypothesis b*k + i */
+        const int h = (int)(r % H);
+        const long hyp = r / H;
+        const int b = (int)(hyp / k);
+        const double *qrow = q + r * D;
+        double *orow = out + r * D;
+        const double *Kpbh = Kp + ((size_t)b * H + h) * (size_t)N * D;
+        const double *Vpbh = Vp + ((size_t)b * H + h) * (size_t)N * D;
+        const double *Ktr = Kt + ((size_t)hyp * H + h) * (size_t)T * D;
+        const double *Vtr = Vt + ((size_t)hyp * H + h) * (size_t)T * D;
+
+        int P = prefix_len[b];
+        if (P < 0) P = 0;
+        if (P > N) P = N;
+        const int n_all = P + t;
+        if (n_all == 0) {
+            for (int d = 0; d < D; ++d) orow[d] = 0.0;
+            continue;
+        }
+        double *w = (double *)malloc(sizeof(double) * (size_t)n_all);
+        if (!w) abort();
+
+        /* attn_w0: scores against the shared prefix */
+        for (int j = 0; j < P; ++j) {
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d)
+                dot += qrow[d] * Kpbh[(size_t)j * D + d];
+            w[j] = dot;
+        }
+        /* attn_w1: scores against this beam's generated tokens */
+        for (int j = 0; j < t; ++j) {
+            double dot = 0.0;
+            for (int d = 0; d < D; ++d)
+                dot += qrow[d] * Ktr[(size_t)j * D + d];
+            w[P + j] = dot;
+        }
+        /* attn_prob = softmax(concat(attn_w0, attn_w1) / sqrt(d)) */
+        for (int j = 0; j < n_all; ++j)
+            w[j] /= root_d;
+        double m = w[0];
+        for (int j = 1; j < n_all; ++j)
+            if (w[j] > m) m = w[j];
+        double Z = 0.0;
+        for (int j = 0; j < n_all; ++j) {
+            w[j] = exp(w[j] - m);
+            Z += w[j];
+        }
+        for (int j = 0; j < n_all; ++j)
+            w[j] /= Z;
+        /* split; attn_t = attn_prob_0 . Cache_V' + attn_prob_1 . V_t */
+        for (int d = 0; d < D; ++d) {
+            double a0 = 0.0, a1 = 0.0;
+            for (int j = 0; j < P; ++j)
+                a0 += w[j] * Vpbh[(size_t)j * D + d];
+            for (int j = 0; j < t; ++j)
+                a1 += w[P + j] * Vtr[(size_t)j * D + d];
+            orow[d] = a0 + a1;
         }
         free(w);
     }

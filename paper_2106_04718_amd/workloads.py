@@ -82,6 +82,64 @@ CONFIGS = {
 }
 
 
+@dataclasses.dataclass(frozen=True)
+class PrefixConfig:
+    """Self-attention step over a split cache: a shared prefix of up to N
+    tokens per sample ([B,H,N,D]) and t generated tokens per beam
+    ([B*k,H,T,D], T the capacity)."""
+    name: str
+    index: int
+    B: int
+    k: int
+    H: int
+    D: int
+    N: int
+    len_lo: int
+    len_hi: int
+    T: int
+    t: int
+    dtype: str
+    sigma: float
+
+    @property
+    def esize(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+
+PREFIX_CONFIGS = {
+    # GPT2-shaped decoder-only summarisation step (12 heads x 64): the
+    # article is the shared prefix, beam 4, generated length up to 140.
+    "gpt2": PrefixConfig("gpt2", 10, B=16, k=4, H=12, D=64, N=1024, len_lo=400, len_hi=1024,
+                         T=140, t=64, dtype="bf16", sigma=1.0),
+    "tiny_prefix": PrefixConfig("tiny_prefix", 11, B=2, k=3, H=2, D=16, N=40, len_lo=1, len_hi=40,
+                                T=24, t=9, dtype="f32", sigma=1.0),
+}
+
+
+def prefix_inputs(cfg, rep: int = 0, pad: str = "zero") -> dict:
+    """q [B,k,H,D], Kp/Vp [B,H,N,D] + prefix_len [B], Kt/Vt [B*k,H,T,D], t.
+
+    Rows j >= prefix_len[b] of Kp/Vp and rows j >= t of Kt/Vt hold ``pad``
+    ("zero" or "nan").  K/V of ``rep`` >= 1 come from their own streams.
+    """
+    if isinstance(cfg, str):
+        cfg = PREFIX_CONFIGS[cfg]
+    st = streams(cfg.index)
+    lens = st[0].integers(cfg.len_lo, cfg.len_hi + 1, size=cfg.B).astype(np.int32)
+    q = _normal(st[1], (cfg.B, cfg.k, cfg.H, cfg.D), cfg.sigma, cfg.dtype)
+    kst, vst = (st[2], st[3]) if rep == 0 else streams(cfg.index, rep)[2:4]
+    Kp = _normal(kst, (cfg.B, cfg.H, cfg.N, cfg.D), cfg.sigma, cfg.dtype)
+    Vp = _normal(vst, (cfg.B, cfg.H, cfg.N, cfg.D), cfg.sigma, cfg.dtype)
+    Kt = _normal(kst, (cfg.B * cfg.k, cfg.H, cfg.T, cfg.D), cfg.sigma, cfg.dtype)
+    Vt = _normal(vst, (cfg.B * cfg.k, cfg.H, cfg.T, cfg.D), cfg.sigma, cfg.dtype)
+    fill_padding(Kp, lens, pad)
+    fill_padding(Vp, lens, pad)
+    tl = np.full(cfg.B * cfg.k, cfg.t, dtype=np.int32)
+    fill_padding(Kt, tl, pad)
+    fill_padding(Vt, tl, pad)
+    return {"q": q, "Kp": Kp, "Vp": Vp, "prefix_len": lens, "Kt": Kt, "Vt": Vt, "t": cfg.t}
+
+
 def get(name_or_index) -> Config:
     if isinstance(name_or_index, Config):
         return name_or_index
@@ -93,9 +151,12 @@ def get(name_or_index) -> Config:
     return CONFIGS[name_or_index]
 
 
-def streams(cfg: Config, rep: int = 0) -> list:
-    """Six independent generators: lengths, q, K, V, tokens, logits."""
-    key = [SEED_BASE, cfg.index] if rep == 0 else [SEED_BASE, cfg.index, rep]
+def streams(cfg, rep: int = 0) -> list:
+    """Six independent generators: lengths, q, K, V, tokens, logits.
+
+    ``cfg`` is a config or its index."""
+    index = cfg if isinstance(cfg, int) else cfg.index
+    key = [SEED_BASE, index] if rep == 0 else [SEED_BASE, index, rep]
     return [np.random.default_rng(s) for s in np.random.SeedSequence(key).spawn(6)]
 
 
