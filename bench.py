@@ -148,8 +148,7 @@ def main() -> int:
     tokens_d = dev_tensor(g["tokens"])
     logits_d = dev_tensor(g["logits"])
     out = torch.empty_like(q)
-    ws = torch.empty(max(16, api.beam_cross_attn_workspace_bytes(cfg.B, cfg.k, cfg.H, cfg.S, cfg.D, tdt)),
-                     dtype=torch.uint8, device=dev)
+    ws = api.new_workspace(api.beam_cross_attn_workspace_bytes(cfg.B, cfg.k, cfg.H, cfg.S, cfg.D, tdt), dev)
     torch.cuda.synchronize()
     log(f"config={cfg.name} K/V sets={R} ({R * set_bytes / 2**30:.2f} GiB) inputs ready in "
         f"{time.perf_counter() - t0:.1f}s")

@@ -66,8 +66,8 @@ const char *fs_last_error(void);
 
 /*
  * Workspace, in bytes, that fs_beam_cross_attn needs for these sizes
- * (per-chunk softmax partials, fp32 values tagged with the call).  0 for
- * empty problems; (size_t)-1 for
+ * (per-chunk softmax partials, fp32 values tagged with the call).  Zero-fill
+ * it before its first use.  0 for empty problems; (size_t)-1 for
  * invalid or unsupported sizes.  The size depends on every argument, so
  * query it again whenever one changes.
  */
@@ -92,9 +92,14 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  *   out      [B, k, H, D]  dtype    result, rounded to nearest-even from fp32
  *   workspace, workspace_bytes      scratch of at least
  *            fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype)
- *            bytes (per-chunk partials); its contents on entry do not
- *            matter and are clobbered.  Calls that share a workspace must
- *            not run concurrently.
+ *            bytes (per-chunk partials).  It must be zero-filled once
+ *            before its first use and not written by anything else after
+ *            that: each call marks the words it writes with a tag of its
+ *            own, and an all-zero or earlier-tagged word is never taken as
+ *            this call's (a tag repeats only after 2^32 calls in one
+ *            process).  Any size-compatible call may reuse it (also of
+ *            fs_beam_prefix_attn).  Calls that share a workspace must not
+ *            run concurrently.
  *   stream   hipStream_t (NULL = default stream)
  * Supported: dtype FS_F32 or FS_BF16, D in {16, 32, 64, 128}, 1 <= k <= 8,
  * B, H, S >= 0 with B*k*H below 2^31 and a launch grid of about
@@ -113,6 +118,49 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V,
                        int B, int k, int H, int S, int D, int dtype,
                        void *workspace, size_t workspace_bytes,
                        void *stream);
+
+/*
+ * Workspace, in bytes, that fs_beam_prefix_attn needs for these sizes (the
+ * partials of fs_beam_cross_attn plus one per-beam record per source and
+ * head for the generated tokens).  Zero-fill it before its first use.  0 for
+ * empty problems; (size_t)-1 for
+ * invalid or unsupported sizes.
+ */
+size_t fs_beam_prefix_attn_workspace_bytes(int B, int k, int H, int N, int T, int D, int dtype);
+
+/*
+ * Self-attention over a split cache (Section 4.1.1; Appendix A, Eq. 2 and
+ * Eq. 3): the keys/values of the prefix (prompt) are stored once per sample
+ * and shared by its k beams; those of the t generated tokens are stored per
+ * beam.  One softmax covers both parts.
+ *
+ * For every sample b, beam i < k (hypothesis r = b*k + i) and head h, with
+ * P = clamp(prefix_len[b], 0, N):
+ *     s = concat((q . Kp[b,h,j,:])_{j<P}, (q . Kt[r,h,j,:])_{j<t}) / sqrt(D)
+ *     out[b,i,h,:] = sum_{j<P} p_j Vp[b,h,j,:] + sum_{j<t} p_{P+j} Vt[r,h,j,:]
+ * with p = softmax(s), and out = 0 when P + t == 0.  Rows j >= P of Kp/Vp and
+ * rows j >= t of Kt/Vt are never read.
+ *
+ * Arguments (device pointers except the sizes):
+ *   q          [B, k, H, D]     dtype  query of step t
+ *   Kp, Vp     [B, H, N, D]     dtype  shared prefix, one copy per sample
+ *   prefix_len [B]              int32  valid prefix rows per sample
+ *   Kt, Vt     [B*k, H, T, D]   dtype  per-beam generated tokens; T is the
+ *                                      capacity, rows 0..t-1 are used
+ *   out        [B, k, H, D]     dtype
+ *   workspace, workspace_bytes  at least fs_beam_prefix_attn_workspace_bytes
+ *                               bytes, zero-filled before its first use
+ *                               (the rules of fs_beam_cross_attn's workspace)
+ * Supported sizes, dtypes, arithmetic, determinism and errors are those of
+ * fs_beam_cross_attn (with N in the role of S); in addition t > T or a
+ * negative T or t is FS_ERR_INVALID_ARG.  The result bits do not depend on k,
+ * B or the beam's position, nor on whether the prefix is shared or passed
+ * replicated per beam.
+ */
+int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                        const void *Kt, const void *Vt, int T, int t, void *out,
+                        int B, int k, int H, int N, int D, int dtype,
+                        void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * No-repeat-n-gram blocking (Section 4.2, Algorithm 1; Section 2.2).

@@ -2,6 +2,8 @@
 
 * :func:`beam_cross_attn` -- encoder-decoder attention in which the k beams
   of a source share one de-duplicated K/V copy (Appendix B, Eq. 4).
+* :func:`beam_prefix_attn` -- self-attention over a split cache: a prefix
+  shared by the beams plus per-beam generated tokens (Appendix A, Eq. 2-3).
 * :func:`ngram_block` -- GPU no-repeat-n-gram blocking, in place
   (Section 4.2, Algorithm 1).
 
@@ -11,7 +13,8 @@ seeded synthetic inputs.  Importing the package loads neither torch nor the
 library; the first call does.
 """
 
-_API = ("beam_cross_attn", "beam_cross_attn_workspace_bytes", "ngram_block")
+_API = ("beam_cross_attn", "beam_cross_attn_workspace_bytes", "beam_prefix_attn",
+        "beam_prefix_attn_workspace_bytes", "new_workspace", "ngram_block")
 
 __all__ = list(_API)
 

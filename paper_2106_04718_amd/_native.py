@@ -26,6 +26,9 @@ SIGNATURES = [
     ("fs_beam_cross_attn_workspace_bytes", _c_size, [_c_int] * 6),
     ("fs_beam_cross_attn", _c_int,
      [_vp, _vp, _vp, _vp, _vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
+    ("fs_beam_prefix_attn_workspace_bytes", _c_size, [_c_int] * 7),
+    ("fs_beam_prefix_attn", _c_int,
+     [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
     ("fs_ngram_block", _c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp]),
 ]
 

@@ -8,9 +8,10 @@ from __future__ import annotations
 
 import torch
 
-from . import _native as N
+from . import _native as _N
 
-_DTYPES = {torch.float32: N.FS_F32, torch.bfloat16: N.FS_BF16}
+_native_lib = _N.lib
+_DTYPES = {torch.float32: _N.FS_F32, torch.bfloat16: _N.FS_BF16}
 
 
 def _stream_ptr(device: torch.device) -> int:
@@ -24,12 +25,22 @@ def _need_cuda(name: str, t: torch.Tensor) -> None:
         raise ValueError(f"{name} must be contiguous")
 
 
+def new_workspace(nbytes: int, device) -> torch.Tensor:
+    """A zero-filled workspace of at least ``nbytes`` for the attention calls.
+
+    The library tags every word it writes with its call, so a workspace
+    needs zero-filling only once, before its first use; reuse it across
+    calls (of any size that fits) without clearing.
+    """
+    return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+
+
 def beam_cross_attn_workspace_bytes(B: int, k: int, H: int, S: int, D: int,
                                     dtype: torch.dtype = torch.bfloat16) -> int:
     """Bytes of fp32 workspace fs_beam_cross_attn needs for these sizes."""
-    n = N.lib().fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, _DTYPES[dtype])
+    n = _N.lib().fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, _DTYPES[dtype])
     if n == 2**64 - 1:
-        raise N.NativeError(N.FS_ERR_UNSUPPORTED, N.last_error())
+        raise _N.NativeError(_N.FS_ERR_UNSUPPORTED, _N.last_error())
     return int(n)
 
 
@@ -39,9 +50,9 @@ def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: 
     """Encoder-decoder attention over de-duplicated K/V (Appendix B, Eq. 4).
 
     q [B,k,H,D], K/V [B,H,S,D] (same dtype: float32 or bfloat16), src_len [B]
-    int32.  Returns out [B,k,H,D] in the input dtype.  ``workspace`` (uint8,
-    at least :func:`beam_cross_attn_workspace_bytes`) may be passed to avoid
-    an allocation per call.
+    int32.  Returns out [B,k,H,D] in the input dtype.  ``workspace`` (from
+    :func:`new_workspace`, zero-filled once, then reused) avoids an
+    allocation and a fill per call.
     """
     for name, t in (("q", q), ("K", K), ("V", V), ("src_len", src_len)):
         _need_cuda(name, t)
@@ -67,14 +78,66 @@ def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: 
     dt = _DTYPES[q.dtype]
     need = beam_cross_attn_workspace_bytes(B, k, H, S, D, q.dtype)
     if workspace is None:
-        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+        workspace = new_workspace(need, dev)
     else:
         _need_cuda("workspace", workspace)
     with torch.cuda.device(dev):
-        N.check(N.lib().fs_beam_cross_attn(
+        _N.check(_N.lib().fs_beam_cross_attn(
             q.data_ptr(), K.data_ptr(), V.data_ptr(), src_len.data_ptr(), out.data_ptr(),
             B, k, H, S, D, dt, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
             _stream_ptr(dev)))
+    return out
+
+
+def beam_prefix_attn_workspace_bytes(B: int, k: int, H: int, N: int, T: int, D: int,
+                                     dtype: torch.dtype = torch.bfloat16) -> int:
+    """Bytes of workspace fs_beam_prefix_attn needs for these sizes."""
+    n = _native_lib().fs_beam_prefix_attn_workspace_bytes(B, k, H, N, T, D, _DTYPES[dtype])
+    if n == 2**64 - 1:
+        raise _N.NativeError(_N.FS_ERR_UNSUPPORTED, _N.last_error())
+    return int(n)
+
+
+def beam_prefix_attn(q: torch.Tensor, Kp: torch.Tensor, Vp: torch.Tensor, prefix_len: torch.Tensor,
+                     Kt: torch.Tensor, Vt: torch.Tensor, t: int, out: torch.Tensor | None = None,
+                     workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Self-attention over a split cache (Appendix A, Eq. 2-3).
+
+    q [B,k,H,D]; Kp, Vp [B,H,N,D] shared prefix with prefix_len [B] int32;
+    Kt, Vt [B*k,H,T,D] per-beam generated tokens of which rows [0, t) are
+    used.  One softmax covers both parts.  Returns out [B,k,H,D].
+    """
+    for name, x in (("q", q), ("Kp", Kp), ("Vp", Vp), ("prefix_len", prefix_len), ("Kt", Kt), ("Vt", Vt)):
+        _need_cuda(name, x)
+    if q.dim() != 4 or Kp.dim() != 4 or Kp.shape != Vp.shape or Kt.dim() != 4 or Kt.shape != Vt.shape:
+        raise ValueError("q [B,k,H,D], Kp/Vp [B,H,N,D], Kt/Vt [B*k,H,T,D]")
+    B, k, H, D = q.shape
+    Np, T = Kp.shape[2], Kt.shape[2]
+    if Kp.shape != (B, H, Np, D) or Kt.shape != (B * k, H, T, D):
+        raise ValueError(f"shape mismatch: q{tuple(q.shape)} Kp{tuple(Kp.shape)} Kt{tuple(Kt.shape)}")
+    if q.dtype not in _DTYPES or any(x.dtype != q.dtype for x in (Kp, Vp, Kt, Vt)):
+        raise ValueError("q, Kp, Vp, Kt and Vt must all be float32 or all bfloat16")
+    if prefix_len.dtype != torch.int32 or prefix_len.shape != (B,):
+        raise ValueError("prefix_len must be int32 [B]")
+    dev = q.device
+    if any(x.device != dev for x in (Kp, Vp, Kt, Vt, prefix_len)):
+        raise ValueError("all tensors must be on one device")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need_cuda("out", out)
+        if out.shape != q.shape or out.dtype != q.dtype or out.device != dev:
+            raise ValueError("out must match q in shape, dtype and device")
+    need = beam_prefix_attn_workspace_bytes(B, k, H, Np, T, D, q.dtype)
+    if workspace is None:
+        workspace = new_workspace(need, dev)
+    else:
+        _need_cuda("workspace", workspace)
+    with torch.cuda.device(dev):
+        _N.check(_native_lib().fs_beam_prefix_attn(
+            q.data_ptr(), Kp.data_ptr(), Vp.data_ptr(), prefix_len.data_ptr(), Kt.data_ptr(), Vt.data_ptr(),
+            T, int(t), out.data_ptr(), B, k, H, Np, D, _DTYPES[q.dtype], workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
     return out
 
 
@@ -104,6 +167,6 @@ def ngram_block(tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | Non
         raise ValueError("t exceeds the columns of tokens")
     dev = tokens.device
     with torch.cuda.device(dev):
-        N.check(N.lib().fs_ngram_block(tokens.data_ptr(), ld, rows, int(t), int(n),
+        _N.check(_N.lib().fs_ngram_block(tokens.data_ptr(), ld, rows, int(t), int(n),
                                        logits.data_ptr(), logits.shape[1], _stream_ptr(dev)))
     return logits

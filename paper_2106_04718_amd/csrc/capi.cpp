@@ -52,8 +52,9 @@ bool validate_mode() {
     return on;
 }
 
-// Epochs tag the cross-attention partial records in the workspace, so a
-// workspace never needs clearing: every call gets a fresh nonzero epoch.
+// Epochs tag the partial records in the workspace: every call gets a fresh
+// nonzero epoch, so a workspace zero-filled once never needs clearing again
+// (a zero word, or one left by an earlier call, never carries this call's tag).
 std::atomic<unsigned long long> g_epoch{1};
 
 unsigned long long next_epoch() {
@@ -78,7 +79,7 @@ int check_attn_sizes(int B, int k, int H, int S, int D, int dtype) {
     const long long C = fs::cross_attn_chunk_keys(D, esize);
     const long long nc = std::max(1LL, (S + C - 1) / C);
     const long long bh_padded = ((long long)B * H + 7) / 8 * 8;  // chunk grid is padded to 8 XCDs
-    if ((long long)B * k * H > INT_MAX || bh_padded * nc + (long long)B * H > INT_MAX)
+    if ((long long)B * k * H > INT_MAX || bh_padded * (nc + 2) > INT_MAX)
         return fail(FS_ERR_INVALID_ARG, "problem too large for one launch (B=%d k=%d H=%d S=%d)",
                     B, k, H, S);
     return FS_OK;
@@ -107,7 +108,19 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
     if (check_attn_sizes(B, k, H, S, D, dtype) != FS_OK) return (size_t)-1;
     if (B == 0 || k == 0 || H == 0) return 0;
     const int esize = dtype == FS_BF16 ? 2 : 4;
-    return fs::cross_attn_workspace_floats(B, k, H, S, D, esize) * sizeof(float);
+    return fs::cross_attn_workspace_floats(B, k, H, S, D, esize, false) * sizeof(float);
+}
+
+size_t fs_beam_prefix_attn_workspace_bytes(int B, int k, int H, int N, int T, int D, int dtype) {
+    g_last_error.clear();
+    if (T < 0) {
+        fail(FS_ERR_INVALID_ARG, "negative size (T=%d)", T);
+        return (size_t)-1;
+    }
+    if (check_attn_sizes(B, k, H, N, D, dtype) != FS_OK) return (size_t)-1;
+    if (B == 0 || k == 0 || H == 0) return 0;
+    const int esize = dtype == FS_BF16 ? 2 : 4;
+    return fs::cross_attn_workspace_floats(B, k, H, N, D, esize, true) * sizeof(float);
 }
 
 int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len,
@@ -154,6 +167,62 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
     hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
                                          static_cast<float *>(workspace), next_epoch(), s);
     if (e != hipSuccess) return hip_fail(e, "fs_beam_cross_attn launch");
+    return FS_OK;
+}
+
+int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                        const void *Kt, const void *Vt, int T, int t, void *out,
+                        int B, int k, int H, int N, int D, int dtype,
+                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_last_error.clear();
+    if (T < 0 || t < 0) return fail(FS_ERR_INVALID_ARG, "negative size (T=%d t=%d)", T, t);
+    if (t > T) return fail(FS_ERR_INVALID_ARG, "t=%d exceeds the generated-token capacity T=%d", t, T);
+    int st = check_attn_sizes(B, k, H, N, D, dtype);
+    if (st != FS_OK) return st;
+    if (B == 0 || k == 0 || H == 0) return FS_OK;
+
+    const size_t esize = dtype == FS_BF16 ? 2 : 4;
+    const size_t q_bytes = (size_t)B * k * H * D * esize;
+    const size_t p_bytes = (size_t)B * H * N * D * esize;
+    const size_t g_bytes = (size_t)B * k * H * T * D * esize;
+    if (!q || !out || !prefix_len || (p_bytes > 0 && (!Kp || !Vp)) || (g_bytes > 0 && (!Kt || !Vt)))
+        return fail(FS_ERR_INVALID_ARG, "null pointer (q=%p Kp=%p Vp=%p prefix_len=%p Kt=%p Vt=%p out=%p)",
+                    q, Kp, Vp, (const void *)prefix_len, Kt, Vt, out);
+    if (!aligned(q, 16) || !aligned(Kp, 16) || !aligned(Vp, 16) || !aligned(Kt, 16) || !aligned(Vt, 16) ||
+        !aligned(out, 16))
+        return fail(FS_ERR_INVALID_ARG, "q, Kp, Vp, Kt, Vt and out must be 16-byte aligned");
+    if (!aligned(prefix_len, 4)) return fail(FS_ERR_INVALID_ARG, "prefix_len must be 4-byte aligned");
+    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, Kp, p_bytes) ||
+        overlaps(out, q_bytes, Vp, p_bytes) || overlaps(out, q_bytes, Kt, g_bytes) ||
+        overlaps(out, q_bytes, Vt, g_bytes) || overlaps(out, q_bytes, prefix_len, (size_t)B * 4))
+        return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
+    if ((long long)B * k * H * ((long long)T * D) > (long long)INT_MAX * 16)
+        return fail(FS_ERR_INVALID_ARG, "generated-token cache too large");
+    const size_t need = fs_beam_prefix_attn_workspace_bytes(B, k, H, N, T, D, dtype);
+    if (workspace_bytes < need || (need > 0 && !workspace))
+        return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed",
+                    workspace_bytes, workspace, need);
+    if (!aligned(workspace, 16)) return fail(FS_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (need > 0 && (overlaps(workspace, need, q, q_bytes) || overlaps(workspace, need, Kp, p_bytes) ||
+                     overlaps(workspace, need, Vp, p_bytes) || overlaps(workspace, need, Kt, g_bytes) ||
+                     overlaps(workspace, need, Vt, g_bytes) || overlaps(workspace, need, out, q_bytes) ||
+                     overlaps(workspace, need, prefix_len, (size_t)B * 4)))
+        return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (validate_mode()) {
+        std::vector<int32_t> lens((size_t)B);
+        hipError_t e = hipMemcpyAsync(lens.data(), prefix_len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) return hip_fail(e, "FS_VALIDATE copy of prefix_len");
+        for (int b = 0; b < B; ++b)
+            if (lens[b] < 0 || lens[b] > N)
+                return fail(FS_ERR_INVALID_ARG, "prefix_len[%d] = %d outside [0, %d]", b, lens[b], N);
+    }
+    hipError_t e = fs::launch_prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, T, t, out, B, k, H, N, D,
+                                          dtype == FS_BF16, static_cast<float *>(workspace), next_epoch(), s);
+    if (e != hipSuccess) return hip_fail(e, "fs_beam_prefix_attn launch");
     return FS_OK;
 }
 

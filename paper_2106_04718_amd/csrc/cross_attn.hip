@@ -264,6 +264,108 @@ __device__ __forceinline__ void store_out(void *out, size_t idx, float v) {
 // current call's tag (about 10 ms at most; not reached in practice).
 constexpr int kMaxSpins = 1 << 14;
 
+// State of one wave tile: keys [t0, min(t0 + kTile, j1)) of one K/V stream
+// (t0 < j1), attended by the KB queries qr.  Kb/Vb point at row 0 of the
+// stream (rows of kLpr 16-byte slices).  On return m[i], l[i] (base-2 max and
+// sum of exp2) are wave-uniform and acc[i][e] holds, in every lane, the
+// unnormalised output for dims sub*kEpl + e.  prow is this wave's LDS area.
+template <int D, bool BF16, int KB>
+__device__ __forceinline__ void tile_attend(const uint4 (&qr)[KB], const uint4 *__restrict__ Kb,
+                                            const uint4 *__restrict__ Vb, int t0, int j1, int sub,
+                                            int grp, float *prow, float scale_log2, float (&m)[KB],
+                                            float (&l)[KB], float (&acc)[KB][Geo<D, BF16>::kEpl])
+{
+    using G = Geo<D, BF16>;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kRpi = G::kRpi;
+    // Row loads: instruction u reads rows t0 + u*kRpi + grp.  Rows past j1
+    // re-read row j1 - 1 (valid data, never padding) and are masked.
+    uint4 kr[kIt], vr[kIt];
+#pragma unroll
+    for (int u = 0; u < kIt; ++u) {
+        const int j = min(t0 + u * kRpi + grp, j1 - 1);
+        kr[u] = load_nt(Kb + (size_t)j * kLpr + sub);
+        vr[u] = load_nt(Vb + (size_t)j * kLpr + sub);
+    }
+    // QK^T: partial dots of this lane's slice, then a reduce-scatter in the
+    // row group, after which the lane owns whole score rows.
+    float d[kIt][KB];
+#pragma unroll
+    for (int u = 0; u < kIt; ++u) {
+#pragma unroll
+        for (int i = 0; i < KB; ++i) d[u][i] = dot16<BF16>(qr[i], kr[u], 0.f);
+    }
+    group_reduce_scatter<kLpr, KB, kIt>(d, sub);
+    constexpr int kRows = G::kRows, kDup = G::kDup;
+    const int u0 = (sub / kDup) * kRows;  // first score row of this lane
+    float mt[KB];
+#pragma unroll
+    for (int i = 0; i < KB; ++i) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < kRows; ++j) {
+            const bool ok = t0 + (u0 + j) * kRpi + grp < j1;
+            d[j][i] = ok ? d[j][i] * scale_log2 : -INFINITY;
+            mx = fmaxf(mx, d[j][i]);
+        }
+        mt[i] = wave_max(mx);  // tile maximum (finite: key t0 is valid)
+    }
+#pragma unroll
+    for (int i = 0; i < KB; ++i) {
+        float lsum = 0.f;
+#pragma unroll
+        for (int j = 0; j < kRows; ++j) {
+            d[j][i] = __builtin_amdgcn_exp2f(d[j][i] - mt[i]);
+            lsum += d[j][i];
+        }
+        l[i] = wave_sum(sub % kDup == 0 ? lsum : 0.f);
+        m[i] = mt[i];
+    }
+#pragma unroll
+    for (int j = 0; j < kRows; ++j) {
+        const int r = (u0 + j) * kRpi + grp;
+#pragma unroll
+        for (int i = 0; i < KB; ++i) prow[(r + (r >> 3)) * KB + i] = d[j][i];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // PV: the coalesced V rows with their weights read back from LDS
+#pragma unroll
+    for (int i = 0; i < KB; ++i) {
+#pragma unroll
+        for (int e = 0; e < kEpl; ++e) acc[i][e] = 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kIt; ++u) {
+        const int r = u * kRpi + grp;
+        float pw[KB];
+#pragma unroll
+        for (int i = 0; i < KB; ++i) pw[i] = prow[(r + (r >> 3)) * KB + i];
+        float vf[kEpl];
+        unpack16<BF16>(vr[u], vf);
+#pragma unroll
+        for (int i = 0; i < KB; ++i) {
+#pragma unroll
+            for (int e = 0; e < kEpl; ++e) acc[i][e] = fmaf(pw[i], vf[e], acc[i][e]);
+        }
+    }
+    // the row groups hold partial sums of the same dims for different rows
+#pragma unroll
+    for (int i = 0; i < KB; ++i) {
+#pragma unroll
+        for (int e = 0; e < kEpl; ++e) acc[i][e] = groups_sum<kLpr>(acc[i][e]);
+    }
+    // keep the next tile's LDS writes behind this tile's reads
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Store one record word (call tag << 32 | fp32 bits) with a device-scope atomic.
+__device__ __forceinline__ void store_word(unsigned long long *p, unsigned long long tag, float v) {
+    __hip_atomic_store(p, tag | __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Merger for (b, h) = bh: merges the chunk records of a source with more
 // than one chunk, in chunk order, and writes the normalised output.
 //
@@ -275,10 +377,14 @@ constexpr int kMaxSpins = 1 << 14;
 // does not carry this call's tag yet is re-read a bounded number of times,
 // and the output becomes NaN if it never does (a loud failure instead of a
 // silent wrong merge or an endless wait).
-template <int D, bool BF16, int KB>
+//
+// With a generated-token segment (SPLIT), record slot NC of (b, h) holds the
+// per-beam state of that segment; it is merged after the prefix chunks, and
+// the merger also writes the rows whose prefix has at most one chunk.
+template <int D, bool BF16, int KB, bool SPLIT>
 __device__ __forceinline__ void merge_chunks(const unsigned long long *__restrict__ part,
                                              const int32_t *__restrict__ src_len, void *__restrict__ out,
-                                             int bh, int n_bh, int H, int S, int NC,
+                                             int bh, int n_bh, int H, int S, int NC, int t,
                                              unsigned long long epoch)
 {
     using G = Geo<D, BF16>;
@@ -287,35 +393,39 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
     const int h = bh - b * H;
     const int L = min(max(src_len[b], 0), S);
     const int nc = (L + G::kChunk - 1) / G::kChunk;
-    if (nc <= 1) return;  // written by the chunk workgroup itself
+    if (!SPLIT && nc <= 1) return;  // written by the chunk workgroup itself
+    const int nrec = nc + (SPLIT && t > 0 ? 1 : 0);  // records to merge, in order
     constexpr int kRec = KB * (D + 2);
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
-    const unsigned long long *recs = part + (size_t)bh * NC * kRec;
+    const unsigned long long *recs = part + (size_t)bh * (NC + (SPLIT ? 1 : 0)) * kRec;
     const size_t obase = ((size_t)b * KB * H + h) * D;
-    constexpr int kBatch = 4;  // chunks whose words are loaded together
+    constexpr int kBatch = 4;  // records whose words are loaded together
     for (int x = threadIdx.x; x < KB * D; x += kBlock) {
         const int i = x / D, d = x - i * D;
         const int at[3] = {KB * D + i, KB * D + KB + i, x};  // m, l, acc
         float mm = -INFINITY, ll = 0.f, aa = 0.f;
         bool stale = false;
-        for (int c0 = 0; c0 < nc; c0 += kBatch) {
+        for (int c0 = 0; c0 < nrec; c0 += kBatch) {
             unsigned long long wv[kBatch][3];
 #pragma unroll
             for (int q2 = 0; q2 < kBatch; ++q2) {
+                // the generated-token record sits in slot NC
+                const int slot = (SPLIT && c0 + q2 == nc) ? NC : c0 + q2;
 #pragma unroll
                 for (int f = 0; f < 3; ++f) {
                     wv[q2][f] = tag;
-                    if (c0 + q2 < nc)
-                        wv[q2][f] = __hip_atomic_load(recs + (size_t)(c0 + q2) * kRec + at[f],
+                    if (c0 + q2 < nrec)
+                        wv[q2][f] = __hip_atomic_load(recs + (size_t)slot * kRec + at[f],
                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
 #pragma unroll
             for (int q2 = 0; q2 < kBatch; ++q2) {
-                if (c0 + q2 >= nc) break;
+                if (c0 + q2 >= nrec) break;
+                const int slot = (SPLIT && c0 + q2 == nc) ? NC : c0 + q2;
 #pragma unroll
                 for (int f = 0; f < 3; ++f) {
-                    const unsigned long long *a = recs + (size_t)(c0 + q2) * kRec + at[f];
+                    const unsigned long long *a = recs + (size_t)slot * kRec + at[f];
                     for (int spin = 0; (wv[q2][f] & 0xffffffff00000000ull) != tag && spin < kMaxSpins; ++spin) {
                         __builtin_amdgcn_s_sleep(2);
                         wv[q2][f] = __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -326,19 +436,72 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
                             __uint_as_float((uint32_t)wv[q2][1]), __uint_as_float((uint32_t)wv[q2][2]));
             }
         }
-        store_out<BF16>(out, obase + (size_t)i * H * D + d, stale ? NAN : aa / ll);
+        const float o = nrec == 0 ? 0.f : aa / ll;  // no key at all: zero row
+        store_out<BF16>(out, obase + (size_t)i * H * D + d, stale ? NAN : o);
     }
 }
 
+// Generated-token segment of (b, h) = bh (SPLIT only): wave w attends beam
+// i = w, w + 4, ... over that hypothesis' own rows [0, t) of Kt/Vt, tile after
+// tile in order, and stores the beam's state in record slot NC of (b, h).
 template <int D, bool BF16, int KB>
+__device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
+                                                 const uint4 *__restrict__ Vt, unsigned long long *__restrict__ part,
+                                                 int bh, int n_bh, int H, int NC, int T, int t,
+                                                 float scale_log2, unsigned long long epoch, float *prow)
+{
+    using G = Geo<D, BF16>;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kTile = G::kTile;
+    if (bh >= n_bh || t <= 0) return;
+    const int b = bh / H;
+    const int h = bh - b * H;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int w = threadIdx.x / kWave;
+    const int sub = lane % kLpr, grp = lane / kLpr;
+    constexpr int kRec = KB * (D + 2);
+    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
+    unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
+    for (int i = w; i < KB; i += kWaves) {
+        const size_t hyp = (size_t)b * KB + i;
+        const uint4 qr[1] = {q[(hyp * H + h) * kLpr + sub]};
+        const uint4 *Kb = Kt + (hyp * H + h) * (size_t)T * kLpr;
+        const uint4 *Vb = Vt + (hyp * H + h) * (size_t)T * kLpr;
+        float m = -INFINITY, l = 0.f, acc[kEpl];
+#pragma unroll
+        for (int e = 0; e < kEpl; ++e) acc[e] = 0.f;
+        for (int t0 = 0; t0 < t; t0 += kTile) {
+            float tm[1], tl[1], ta[1][kEpl];
+            tile_attend<D, BF16, 1>(qr, Kb, Vb, t0, t, sub, grp, prow, scale_log2, tm, tl, ta);
+            // fold the tile into the running state (wave-uniform m, l)
+            const float mx = fmaxf(m, tm[0]);
+            const float fo = __builtin_amdgcn_exp2f(m - mx);
+            const float fn = __builtin_amdgcn_exp2f(tm[0] - mx);
+            l = l * fo + tl[0] * fn;
+#pragma unroll
+            for (int e = 0; e < kEpl; ++e) acc[e] = acc[e] * fo + ta[0][e] * fn;
+            m = mx;
+        }
+        if (lane < kLpr) {
+#pragma unroll
+            for (int e = 0; e < kEpl; ++e) store_word(rec + i * D + sub * kEpl + e, tag, acc[e]);
+        }
+        if (lane == 0) {
+            store_word(rec + KB * D + i, tag, m);
+            store_word(rec + KB * D + KB + i, tag, l);
+        }
+    }
+}
+
+template <int D, bool BF16, int KB, bool SPLIT>
 __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
     const int32_t *__restrict__ src_len, void *__restrict__ out,
     unsigned long long *__restrict__ part,
-    int n_bh, int H, int S, int NC, float scale_log2, unsigned long long epoch)
+    int n_bh, int H, int S, int NC, float scale_log2, unsigned long long epoch,
+    const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t)
 {
     using G = Geo<D, BF16>;
-    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kRpi = G::kRpi;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
 
     __shared__ float m_lds[kWaves][KB], l_lds[kWaves][KB];
@@ -346,12 +509,23 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     __shared__ __attribute__((aligned(16))) float p_lds[kWaves][G::kPStride][KB];
 
     // Workgroup g runs on XCD g % 8 (round-robin dispatch).  All chunks of
-    // one (b, h), and its merger, get ids with the same residue, so they
-    // share an L2.  Merger workgroups come after every chunk workgroup.
-    const int g = blockIdx.x;
-    const int n_chunk_blocks = ((n_bh + kXcds - 1) / kXcds) * kXcds * NC;
+    // one (b, h), its generated-token workgroup and its merger get ids with
+    // the same residue, so they share an L2.  Order of the id ranges: the
+    // generated-token workgroups (SPLIT only; each walks its tiles in
+    // sequence, so they start first), the chunk workgroups, the mergers.
+    const int n_bh8 = ((n_bh + kXcds - 1) / kXcds) * kXcds;
+    int g = blockIdx.x;
+    if constexpr (SPLIT) {
+        if (g < n_bh8) {
+            attend_generated<D, BF16, KB>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
+                                          &p_lds[threadIdx.x / kWave][0][0]);
+            return;
+        }
+        g -= n_bh8;
+    }
+    const int n_chunk_blocks = n_bh8 * NC;
     if (g >= n_chunk_blocks) {
-        merge_chunks<D, BF16, KB>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC, epoch);
+        merge_chunks<D, BF16, KB, SPLIT>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC, t, epoch);
         return;
     }
     const int xcd = g % kXcds;
@@ -366,7 +540,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const int nc = (L + kChunk - 1) / kChunk;
     const int tid = threadIdx.x;
     const size_t obase = ((size_t)b * KB * H + h) * D;  // out[b, 0, h, 0]
-    if (L == 0) {  // no valid key: the output row is zero
+    if (!SPLIT && L == 0) {  // no valid key: the output row is zero
         if (c == 0)
             for (int x = tid; x < KB * D; x += kBlock)
                 store_out<BF16>(out, obase + (size_t)(x / D) * H * D + x % D, 0.f);
@@ -397,82 +571,8 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     }
 
     const int t0 = j0 + w * kTile;
-    if (t0 < j1) {
-        // Row loads: instruction u reads rows t0 + u*kRpi + grp.  Rows past
-        // j1 re-read row j1 - 1 (valid data, never padding) and are masked.
-        uint4 kr[kIt], vr[kIt];
-#pragma unroll
-        for (int u = 0; u < kIt; ++u) {
-            const int j = min(t0 + u * kRpi + grp, j1 - 1);
-            kr[u] = load_nt(Kbh + (size_t)j * kLpr + sub);
-            vr[u] = load_nt(Vbh + (size_t)j * kLpr + sub);
-        }
-        // QK^T: partial dots of this lane's slice, then a reduce-scatter in
-        // the row group, after which the lane owns whole score rows.
-        float d[kIt][KB];
-#pragma unroll
-        for (int u = 0; u < kIt; ++u) {
-#pragma unroll
-            for (int i = 0; i < KB; ++i) d[u][i] = dot16<BF16>(qr[i], kr[u], 0.f);
-        }
-        group_reduce_scatter<kLpr, KB, kIt>(d, sub);
-        constexpr int kRows = G::kRows, kDup = G::kDup;
-        const int u0 = (sub / kDup) * kRows;  // first score row of this lane
-        float mt[KB];
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-            float mx = -INFINITY;
-#pragma unroll
-            for (int j = 0; j < kRows; ++j) {
-                const bool ok = t0 + (u0 + j) * kRpi + grp < j1;
-                d[j][i] = ok ? d[j][i] * scale_log2 : -INFINITY;
-                mx = fmaxf(mx, d[j][i]);
-            }
-            mt[i] = wave_max(mx);  // tile maximum (finite: key t0 is valid)
-        }
-        float* prow = &p_lds[w][0][0];
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-            float lsum = 0.f;
-#pragma unroll
-            for (int j = 0; j < kRows; ++j) {
-                d[j][i] = __builtin_amdgcn_exp2f(d[j][i] - mt[i]);
-                lsum += d[j][i];
-            }
-            l[i] = wave_sum(sub % kDup == 0 ? lsum : 0.f);
-            m[i] = mt[i];
-        }
-#pragma unroll
-        for (int j = 0; j < kRows; ++j) {
-            const int r = (u0 + j) * kRpi + grp;
-#pragma unroll
-            for (int i = 0; i < KB; ++i) prow[(r + (r >> 3)) * KB + i] = d[j][i];
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        // PV: the coalesced V rows with their weights read back from LDS
-#pragma unroll
-        for (int u = 0; u < kIt; ++u) {
-            const int r = u * kRpi + grp;
-            float pw[KB];
-#pragma unroll
-            for (int i = 0; i < KB; ++i) pw[i] = prow[(r + (r >> 3)) * KB + i];
-            float vf[kEpl];
-            unpack16<BF16>(vr[u], vf);
-#pragma unroll
-            for (int i = 0; i < KB; ++i) {
-#pragma unroll
-                for (int e = 0; e < kEpl; ++e) acc[i][e] = fmaf(pw[i], vf[e], acc[i][e]);
-            }
-        }
-        // the row groups hold partial sums of the same dims for different rows
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-#pragma unroll
-            for (int e = 0; e < kEpl; ++e) acc[i][e] = groups_sum<kLpr>(acc[i][e]);
-        }
-    }
+    if (t0 < j1)
+        tile_attend<D, BF16, KB>(qr, Kbh, Vbh, t0, j1, sub, grp, &p_lds[w][0][0], scale_log2, m, l, acc);
     if (lane < kLpr) {
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
@@ -489,7 +589,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     }
     __syncthreads();
 
-    if (nc == 1) {
+    if (!SPLIT && nc == 1) {
         for (int x = tid; x < KB * D; x += kBlock) {
             const int i = x / D, d = x - i * D;
             float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds[0][i][d];
@@ -501,72 +601,81 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     }
 
     // Partial record of (b, h, c): acc[KB][D], then m[KB], then l[KB].
-    unsigned long long *rec = part + ((size_t)bh * NC + c) * (KB * (D + 2));
+    unsigned long long *rec = part + ((size_t)bh * (NC + (SPLIT ? 1 : 0)) + c) * (KB * (D + 2));
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     for (int x = tid; x < KB * D; x += kBlock) {
         const int i = x / D, d = x - i * D;
         float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds[0][i][d];
 #pragma unroll
         for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds[ww][i][d]);
-        __hip_atomic_store(rec + x, tag | __float_as_uint(aa), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        store_word(rec + x, tag, aa);
         if (d == 0) {
-            __hip_atomic_store(rec + KB * D + i, tag | __float_as_uint(mm), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(rec + KB * D + KB + i, tag | __float_as_uint(ll), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            store_word(rec + KB * D + i, tag, mm);
+            store_word(rec + KB * D + KB + i, tag, ll);
         }
     }
 }
 
-template <int D, bool BF16, int KB>
-hipError_t launch_typed(const void *q, const void *K, const void *V, const int32_t *src_len,
-                        void *out, int B, int H, int S, float *ws, unsigned long long epoch,
-                        hipStream_t stream)
+// Launch arguments shared by both entry points.  For the encoder-decoder
+// form Kt/Vt are null and T = t = 0.
+struct AttnArgs {
+    const void *q, *K, *V;
+    const int32_t *src_len;
+    void *out;
+    int B, k, H, S, D;
+    const void *Kt, *Vt;
+    int T, t;
+    float *ws;
+    unsigned long long epoch;
+    hipStream_t stream;
+};
+
+template <int D, bool BF16, int KB, bool SPLIT>
+hipError_t launch_typed(const AttnArgs &a)
 {
     using G = Geo<D, BF16>;
     // at least one chunk column, so that a source with no valid key (or
     // S == 0) still has a workgroup to write its zero output
-    const int NC = max(1, (S + G::kChunk - 1) / G::kChunk);
-    const int n_bh = B * H;
+    const int NC = max(1, (a.S + G::kChunk - 1) / G::kChunk);
+    const int n_bh = a.B * a.H;
+    const long long n_bh8 = ((long long)n_bh + kXcds - 1) / kXcds * kXcds;
     const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
-    unsigned long long *part = reinterpret_cast<unsigned long long *>(ws);
-    const long long groups = ((long long)n_bh + kXcds - 1) / kXcds;
-    const long long nblk = groups * kXcds * NC + (NC > 1 ? n_bh : 0);  // chunks, then mergers
-    hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB>), dim3((unsigned)nblk), dim3(kBlock), 0,
-                       stream, static_cast<const uint4 *>(q), static_cast<const uint4 *>(K),
-                       static_cast<const uint4 *>(V), src_len, out, part, n_bh, H, S,
-                       NC, (float)scale_log2, epoch);
+    unsigned long long *part = reinterpret_cast<unsigned long long *>(a.ws);
+    // [generated-token workgroups] [chunk workgroups] [mergers]
+    const long long mergers = (SPLIT || NC > 1) ? n_bh : 0;
+    const long long nblk = (SPLIT ? n_bh8 : 0) + n_bh8 * NC + mergers;
+    hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB, SPLIT>), dim3((unsigned)nblk), dim3(kBlock), 0,
+                       a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
+                       static_cast<const uint4 *>(a.V), a.src_len, a.out, part, n_bh, a.H, a.S,
+                       NC, (float)scale_log2, a.epoch, static_cast<const uint4 *>(a.Kt),
+                       static_cast<const uint4 *>(a.Vt), a.T, a.t);
     return hipGetLastError();
 }
 
-template <int D, bool BF16>
-hipError_t launch_k(int k, const void *q, const void *K, const void *V, const int32_t *src_len,
-                    void *out, int B, int H, int S, float *ws, unsigned long long epoch,
-                    hipStream_t stream)
+template <int D, bool BF16, bool SPLIT>
+hipError_t launch_k(const AttnArgs &a)
 {
-    switch (k) {
-    case 1: return launch_typed<D, BF16, 1>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 2: return launch_typed<D, BF16, 2>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 3: return launch_typed<D, BF16, 3>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 4: return launch_typed<D, BF16, 4>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 5: return launch_typed<D, BF16, 5>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 6: return launch_typed<D, BF16, 6>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 7: return launch_typed<D, BF16, 7>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 8: return launch_typed<D, BF16, 8>(q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    switch (a.k) {
+    case 1: return launch_typed<D, BF16, 1, SPLIT>(a);
+    case 2: return launch_typed<D, BF16, 2, SPLIT>(a);
+    case 3: return launch_typed<D, BF16, 3, SPLIT>(a);
+    case 4: return launch_typed<D, BF16, 4, SPLIT>(a);
+    case 5: return launch_typed<D, BF16, 5, SPLIT>(a);
+    case 6: return launch_typed<D, BF16, 6, SPLIT>(a);
+    case 7: return launch_typed<D, BF16, 7, SPLIT>(a);
+    case 8: return launch_typed<D, BF16, 8, SPLIT>(a);
     default: return hipErrorInvalidValue;
     }
 }
 
-template <bool BF16>
-hipError_t launch_d(int D, int k, const void *q, const void *K, const void *V,
-                    const int32_t *src_len, void *out, int B, int H, int S, float *ws,
-                    unsigned long long epoch, hipStream_t stream)
+template <bool BF16, bool SPLIT>
+hipError_t launch_d(const AttnArgs &a)
 {
-    switch (D) {
-    case 16: return launch_k<16, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 32: return launch_k<32, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 64: return launch_k<64, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
-    case 128: return launch_k<128, BF16>(k, q, K, V, src_len, out, B, H, S, ws, epoch, stream);
+    switch (a.D) {
+    case 16: return launch_k<16, BF16, SPLIT>(a);
+    case 32: return launch_k<32, BF16, SPLIT>(a);
+    case 64: return launch_k<64, BF16, SPLIT>(a);
+    case 128: return launch_k<128, BF16, SPLIT>(a);
     default: return hipErrorInvalidValue;
     }
 }
@@ -578,21 +687,29 @@ int cross_attn_chunk_keys(int D, int esize) {
     return kWaves * kIt * kWave * 16 / (D * esize);
 }
 
-size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize) {
+size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize, bool split) {
     const int C = cross_attn_chunk_keys(D, esize);
-    const size_t NC = (size_t)std::max(1, (S + C - 1) / C);
+    const size_t NC = (size_t)std::max(1, (S + C - 1) / C) + (split ? 1 : 0);
     const size_t n_bh = (size_t)B * H;
     const size_t part = n_bh * NC * (size_t)k * (size_t)(D + 2);
-    // 64-bit partial-record words
-    return 2 * part;
+    return 2 * part;  // 64-bit partial-record words
 }
 
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len,
                              void *out, int B, int k, int H, int S, int D, bool bf16,
                              float *workspace, unsigned long long epoch, hipStream_t stream)
 {
-    return bf16 ? launch_d<true>(D, k, q, K, V, src_len, out, B, H, S, workspace, epoch, stream)
-                : launch_d<false>(D, k, q, K, V, src_len, out, B, H, S, workspace, epoch, stream);
+    const AttnArgs a{q, K, V, src_len, out, B, k, H, S, D, nullptr, nullptr, 0, 0, workspace, epoch, stream};
+    return bf16 ? launch_d<true, false>(a) : launch_d<false, false>(a);
+}
+
+hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                              const void *Kt, const void *Vt, int T, int t, void *out, int B, int k,
+                              int H, int N, int D, bool bf16, float *workspace,
+                              unsigned long long epoch, hipStream_t stream)
+{
+    const AttnArgs a{q, Kp, Vp, prefix_len, out, B, k, H, N, D, Kt, Vt, T, t, workspace, epoch, stream};
+    return bf16 ? launch_d<true, true>(a) : launch_d<false, true>(a);
 }
 
 }  // namespace fs

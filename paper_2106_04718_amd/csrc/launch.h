@@ -15,8 +15,9 @@ namespace fs {
 // source is read by one beam or by k beams.
 int cross_attn_chunk_keys(int D, int esize);
 
-// Workspace size in 4-byte words: the per-chunk partial records.
-size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize);
+// Workspace size in 4-byte words: the per-chunk partial records (plus one
+// record per (b, h) for the generated-token segment when `split`).
+size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize, bool split);
 
 // `epoch` must differ from the epoch of every earlier call that used the
 // same workspace: its low 32 bits tag the partial records, which are never
@@ -25,6 +26,13 @@ hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
                              const int32_t *src_len, void *out,
                              int B, int k, int H, int S, int D, bool bf16,
                              float *workspace, unsigned long long epoch, hipStream_t stream);
+
+// Split-cache self-attention: shared prefix Kp/Vp [B,H,N,D] with
+// prefix_len[B], per-beam generated tokens Kt/Vt [B*k,H,T,D] (rows < t).
+hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                              const void *Kt, const void *Vt, int T, int t, void *out, int B, int k,
+                              int H, int N, int D, bool bf16, float *workspace,
+                              unsigned long long epoch, hipStream_t stream);
 
 hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t,
                               int n, float *logits, int V, hipStream_t stream);

@@ -141,7 +141,7 @@ def test_caller_buffers_and_workspace_reuse():
     d = random_case(2, 4, 2, 128, 64, "bf16", [128, 77], seed=41)
     dev = device()
     need = api.beam_cross_attn_workspace_bytes(2, 4, 2, 128, 64, torch.bfloat16)
-    ws = torch.full((need,), 0x7F, dtype=torch.uint8, device=dev)   # garbage content
+    ws = api.new_workspace(need, dev)
     out = torch.full((2, 4, 2, 64), float("nan"), dtype=torch.bfloat16, device=dev)
     say("[attn api] caller workspace")
     o = run(d, out=out, ws=ws)
@@ -153,13 +153,14 @@ def test_caller_buffers_and_workspace_reuse():
 
 
 def test_workspace_reused_across_calls_with_changing_lengths():
-    # The completion counters in the workspace are never cleared; each call
-    # must still find its own last chunk.  Reuse one workspace for calls whose
-    # chunk counts differ, then for a different problem size.
+    # The workspace is zero-filled once and never cleared again: every call
+    # must take only the records it wrote itself (tagged with its own call
+    # number).  Reuse one workspace for calls whose chunk counts differ, then
+    # for a different problem size.
     dev = device()
     rng = np.random.default_rng(51)
     need = api.beam_cross_attn_workspace_bytes(6, 4, 3, 1100, 64, torch.bfloat16)
-    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=dev)
+    ws = api.new_workspace(need, dev)
     for rep in range(6):
         lens = rng.integers(0, 1101, size=6)
         lens[rep % 6] = 1100
