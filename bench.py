@@ -43,7 +43,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="bart", help="tiny | bart | t5 | prophetnet | large")
+    ap.add_argument("--config", default="bart",
+                    help="decode step: tiny | bart | t5 | prophetnet | large; "
+                         "split-cache self-attention step: gpt2 | tiny_prefix")
     ap.add_argument("--rotate-gib", type=float, default=1.0,
                     help="minimum total size of the rotated K/V sets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -70,6 +72,55 @@ def ngram_bytes(rows: int, t: int, bans: int) -> int:
     """Algorithmic bytes of one n-gram call: the token history is read once;
     each banned logit is one 4-byte store (the logits are never read)."""
     return rows * t * 4 + 4 * bans
+
+
+def prefix_bytes(cfg, lens, t: int) -> int:
+    """Algorithmic bytes of one split-cache self-attention call: the valid
+    prefix rows of K and V once per sample, the t generated rows of every
+    beam, q and out, and prefix_len."""
+    e = cfg.esize
+    kv = 2 * int(sum(int(x) for x in lens)) * cfg.H * cfg.D * e
+    gen = 2 * cfg.B * cfg.k * cfg.H * t * cfg.D * e
+    qo = 2 * cfg.B * cfg.k * cfg.H * cfg.D * e
+    return kv + gen + qo + 4 * cfg.B
+
+
+def launch_spread(stream, fn, K: int, parts: int = 10) -> dict:
+    """Median, p10 and p90 of the mean per-call time of ``fn(i)`` over
+    ``parts`` equal sub-regions of K back-to-back calls (events only at the
+    sub-region ends).  Timed in a pass of its own, so that its extra events
+    never enter the headline means."""
+    import numpy as np
+    import torch
+    per = max(1, K // parts)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(parts + 1)]
+    torch.cuda.synchronize()
+    i = 0
+    ev[0].record(stream)
+    for p in range(parts):
+        for _ in range(per):
+            fn(i)
+            i += 1
+        ev[p + 1].record(stream)
+    torch.cuda.synchronize()
+    us = np.array([ev[p].elapsed_time(ev[p + 1]) * 1e3 / per for p in range(parts)])
+    return {"median": round(float(np.median(us)), 3), "p10": round(float(np.percentile(us, 10)), 3),
+            "p90": round(float(np.percentile(us, 90)), 3), "subregions": parts, "calls_each": per}
+
+
+def load_traffic(path: str, name: str):
+    """HBM bytes per launch from the counter summary, if it was taken on the
+    current kernel sources."""
+    tp = pathlib.Path(path)
+    if not tp.exists():
+        return None
+    try:
+        rec = json.loads(tp.read_text()).get(name)
+    except (ValueError, OSError):
+        return None
+    if rec and rec.get("kernel_source_sha") == kernel_source_sha():
+        return rec.get("bytes_per_launch")
+    return None
 
 
 def copy_bandwidth(dev, gib: float = 1.0, reps: int = 5) -> float:
@@ -121,6 +172,8 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.config in workloads.PREFIX_CONFIGS:
+        return bench_prefix(args, workloads.PREFIX_CONFIGS[args.config], dev)
     cfg = workloads.get(args.config)
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
 
@@ -192,6 +245,9 @@ def main() -> int:
     e[3].record(stream)
     torch.cuda.synchronize()
     ca_us = e[2].elapsed_time(e[3]) * 1e3 / K_
+    step_spread = launch_spread(stream, step, K_)
+    ca_spread = launch_spread(stream, lambda i: api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out,
+                                                                    workspace=ws), K_)
     ms_per_step = region_ms / K_
     step_us = ms_per_step * 1e3
     ng_us = max(step_us - ca_us, 0.0)
@@ -206,15 +262,7 @@ def main() -> int:
         f"{100 * ca_gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s); "
         f"n-gram {ng_us:.2f} us = {100 * ng_us / step_us:.1f}% of the step")
 
-    traffic = None
-    tp = pathlib.Path(args.traffic)
-    if tp.exists():
-        try:
-            rec = json.loads(tp.read_text()).get(cfg.name)
-            if rec and rec.get("kernel_source_sha") == kernel_source_sha():
-                traffic = rec.get("bytes_per_launch")
-        except (ValueError, OSError):
-            traffic = None
+    traffic = load_traffic(args.traffic, cfg.name)
 
     line = {
         "metric": "decode-step µs and achieved HBM GB/s (cross-attn + n-gram block), BART-large shape",
@@ -233,7 +281,9 @@ def main() -> int:
         "config": {"workload": workload_name(cfg), "B": cfg.B, "k": cfg.k, "H": cfg.H, "D": cfg.D,
                    "S": cfg.S, "t": cfg.t, "V": cfg.V, "n": cfg.n, "kv_sets_rotated": R,
                    "bytes_per_step": b_step},
+        "step_us_spread": step_spread,
         "cross_attn_us": round(ca_us, 3),
+        "cross_attn_us_spread": ca_spread,
         "ngram_us": round(ng_us, 3),
         "ngram_share_of_step": round(ng_us / step_us, 4),
         "copy_gbps": round(copy_gbps, 1),
@@ -245,6 +295,117 @@ def main() -> int:
     if not args.no_cpu_baseline:
         line["cpu_baseline"], line["parity"] = cpu_baseline(cfg, base, g, out0, logits0, b_step,
                                                              args.cpu_reps)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def bench_prefix(args, cfg, dev) -> int:
+    """Split-cache self-attention step (decoder-only beam search): each
+    sample's prefix K/V read once for its k beams, plus each beam's own
+    generated K/V, one softmax.  A step is one fs_beam_prefix_attn call."""
+    import numpy as np
+    import torch
+
+    from paper_2106_04718_amd import api, workloads
+
+    def dev_tensor(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    t0 = time.perf_counter()
+    base = workloads.prefix_inputs(cfg)
+    lens, t = base["prefix_len"], base["t"]
+    set_bytes = sum(base[x].nbytes for x in ("Kp", "Vp", "Kt", "Vt"))
+    R = max(1, math.ceil(args.rotate_gib * (1 << 30) / set_bytes))
+    q, lens_d = dev_tensor(base["q"]), dev_tensor(lens)
+    sets = [tuple(dev_tensor(base[x]) for x in ("Kp", "Vp", "Kt", "Vt"))]
+    for r in range(1, R):
+        d = workloads.prefix_inputs(cfg, rep=r)
+        sets.append(tuple(dev_tensor(d[x]) for x in ("Kp", "Vp", "Kt", "Vt")))
+        del d
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_prefix_attn_workspace_bytes(cfg.B, cfg.k, cfg.H, cfg.N, cfg.T, cfg.D, tdt),
+                           dev)
+    torch.cuda.synchronize()
+    log(f"config={cfg.name} K/V sets={R} ({R * set_bytes / 2**30:.2f} GiB) inputs ready in "
+        f"{time.perf_counter() - t0:.1f}s")
+
+    def step(i: int):
+        Kp, Vp, Kt, Vt = sets[i % R]
+        api.beam_prefix_attn(q, Kp, Vp, lens_d, Kt, Vt, t, out=out, workspace=ws)
+
+    step(0)
+    torch.cuda.synchronize()
+    out0 = out.float().cpu().numpy().astype(np.float64)
+    for i in range(args.warmup):
+        step(i)
+    K_ = args.steps
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(K_):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    step_us = e0.elapsed_time(e1) * 1e3 / K_
+    spread = launch_spread(stream, step, K_)
+    b = prefix_bytes(cfg, lens, t)
+    gbps = b / (step_us * 1e-6) / 1e9
+    copy_gbps = copy_bandwidth(dev)
+    log(f"prefix step {step_us:.2f} us = {gbps:.0f} GB/s ({100 * gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
+        f"{100 * gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s)")
+    line = {
+        "metric": "self-attention step µs and achieved HBM GB/s (split-cache prefix attention), GPT2 shape",
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K_,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_us * 1e-3, 6),
+        "step_us": round(step_us, 3),
+        "step_us_spread": spread,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded; shared prefix K/V per sample, per-beam generated K/V)",
+        "config": {"workload": (f"{cfg.name}-shaped split-cache self-attention step: B={cfg.B} k={cfg.k} "
+                                f"H={cfg.H} D={cfg.D}, shared prefix N={cfg.N} (lengths U{{{cfg.len_lo}.."
+                                f"{cfg.len_hi}}}), {t} generated tokens per beam (capacity {cfg.T}), "
+                                f"{cfg.dtype}"),
+                   "B": cfg.B, "k": cfg.k, "H": cfg.H, "D": cfg.D, "N": cfg.N, "T": cfg.T, "t": t,
+                   "kv_sets_rotated": R, "bytes_per_step": b},
+        "copy_gbps": round(copy_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": "fs_beam_prefix_attn", "achieved": round(gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "algorithmic_bytes_per_launch": b, "traffic": load_traffic(args.traffic, cfg.name)},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        qd, Kpd, Vpd, Ktd, Vtd = (np.ascontiguousarray(oracle.widen(base[x]))
+                                  for x in ("q", "Kp", "Vp", "Kt", "Vt"))
+        times, ref = [], None
+        while True:
+            c0 = time.perf_counter()
+            ref = oracle.prefix_attn(qd, Kpd, Vpd, lens, Ktd, Vtd, t)
+            times.append(time.perf_counter() - c0)
+            if (args.cpu_reps and len(times) >= args.cpu_reps) or \
+                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                break
+        sec = float(np.median(times))
+        err = float(np.max(np.abs(out0 - ref)))
+        tol = 2e-2 if cfg.dtype == "bf16" else 1e-5 * float(np.max(np.abs(ref)))
+        log(f"oracle: {sec * 1e3:.1f} ms per step on {oracle.num_threads()} threads; attn max abs err {err:.3e}")
+        line["cpu_baseline"] = {"value": round(b / sec / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
+                                "kind": "oracle",
+                                "sample": f"whole {cfg.name}-shaped step, K/V set 0, median of {len(times)} reps, "
+                                          f"{sec * 1e3:.1f} ms per step"}
+        line["parity"] = {"attn_max_abs_err": err, "attn_tol": tol, "attn_ok": err <= tol}
     print(json.dumps(line), flush=True)
     return 0
 
@@ -273,17 +434,32 @@ def cpu_baseline(cfg, base, g, out0, logits0, step_bytes, reps):
     qd, Kd, Vd = (np.ascontiguousarray(oracle.widen(base[x])) for x in ("q", "K", "V"))
     tokens = np.ascontiguousarray(g["tokens"])
     cores = oracle.num_threads()
-    times = []
+    times, t_attn, t_ng = [], [], []
     ref = None
     while True:
         lg = np.array(g["logits"], copy=True)
         t0 = time.perf_counter()
         ref = oracle.cross_attn_f64(qd, Kd, Vd, base["src_len"])
+        t1 = time.perf_counter()
         oracle.ngram_block_inplace(tokens, cfg.n, lg, cfg.t)
-        times.append(time.perf_counter() - t0)
+        t2 = time.perf_counter()
+        times.append(t2 - t0)
+        t_attn.append(t1 - t0)
+        t_ng.append(t2 - t1)
         if (reps and len(times) >= reps) or (not reps and (sum(times) > 10.0 or len(times) >= 50)):
             break
     sec = float(np.median(times))
+    # One more pass on a single thread, for the per-core figure.
+    oracle.set_num_threads(1)
+    try:
+        lg1 = np.array(g["logits"], copy=True)
+        s0 = time.perf_counter()
+        oracle.cross_attn_f64(qd, Kd, Vd, base["src_len"])
+        s1 = time.perf_counter()
+        oracle.ngram_block_inplace(tokens, cfg.n, lg1, cfg.t)
+        s2 = time.perf_counter()
+    finally:
+        oracle.set_num_threads(cores)
     err = float(np.max(np.abs(out0 - ref)))
     tol = 2e-2 if cfg.dtype == "bf16" else 1e-5 * float(np.max(np.abs(ref)))
     ng_ok = bool(np.array_equal(lg.view(np.uint32), logits0.view(np.uint32)))
@@ -292,7 +468,9 @@ def cpu_baseline(cfg, base, g, out0, logits0, step_bytes, reps):
     cpu = {"value": round(step_bytes / sec / 1e9, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
            "sample": f"whole {cfg.name}-shaped step (all {cfg.B} sources x {cfg.k} beams x {cfg.H} heads, "
                      f"{cfg.rows} token rows), K/V set 0, median of {len(times)} reps, "
-                     f"{sec * 1e3:.1f} ms per step"}
+                     f"{sec * 1e3:.1f} ms per step",
+           "attn_ms": round(float(np.median(t_attn)) * 1e3, 3), "ngram_ms": round(float(np.median(t_ng)) * 1e3, 3),
+           "attn_ms_1thread": round((s1 - s0) * 1e3, 3), "ngram_ms_1thread": round((s2 - s1) * 1e3, 3)}
     parity = {"attn_max_abs_err": err, "attn_tol": tol, "attn_ok": err <= tol, "ngram_bitexact": ng_ok}
     return cpu, parity
 
