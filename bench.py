@@ -42,10 +42,13 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=500,
+                    help="untimed steps first (about 12 ms at the BART shape, enough for the clocks to settle)")
     ap.add_argument("--config", default="bart",
                     help="decode step: tiny | bart | t5 | prophetnet | large; "
                          "split-cache self-attention step: gpt2 | tiny_prefix")
+    ap.add_argument("--rounds", type=int, default=5,
+                    help="alternating (steps, cross-attention only) region pairs for the per-kernel split")
     ap.add_argument("--rotate-gib", type=float, default=1.0,
                     help="minimum total size of the rotated K/V sets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -221,36 +224,39 @@ def main() -> int:
     # ---- warm-up and timed regions -----------------------------------------
     # Region A times exactly K steps with events only at its two ends: event
     # records between kernels would themselves add several microseconds per
-    # step.  Region B times K back-to-back cross-attention launches (same
-    # stream, same K/V rotation) for the kernel's own average duration; the
-    # n-gram step's cost is the difference between the two.
+    # step.  It gives the headline step time.  Then `rounds` pairs of
+    # regions alternate: K steps (A_r) and K back-to-back cross-attention
+    # launches on the same stream with the same K/V rotation (B_r).  The
+    # kernel's average duration is the median of B_r; the n-gram step's cost
+    # is the median of A_r - B_r (pairing cancels slow clock drift).
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     K_ = args.steps
     stream = torch.cuda.current_stream(dev)
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-    torch.cuda.synchronize()
-    w0 = time.perf_counter()
-    e[0].record(stream)
-    for i in range(K_):
-        step(i)
-    e[1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    region_ms = e[0].elapsed_time(e[1])
-    e[2].record(stream)
-    for i in range(K_):
+
+    def ca_only(i: int):
         api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
-    e[3].record(stream)
-    torch.cuda.synchronize()
-    ca_us = e[2].elapsed_time(e[3]) * 1e3 / K_
+
+    def region_us(fn) -> float:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(K_):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / K_
+
+    w0 = time.perf_counter()
+    step_us = region_us(step)
+    wall = time.perf_counter() - w0
+    pairs = [(region_us(step), region_us(ca_only)) for _ in range(max(1, args.rounds))]
+    ca_us = float(np.median([b for _, b in pairs]))
+    ng_us = max(float(np.median([a - b for a, b in pairs])), 0.0)
     step_spread = launch_spread(stream, step, K_)
-    ca_spread = launch_spread(stream, lambda i: api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out,
-                                                                    workspace=ws), K_)
-    ms_per_step = region_ms / K_
-    step_us = ms_per_step * 1e3
-    ng_us = max(step_us - ca_us, 0.0)
+    ca_spread = launch_spread(stream, ca_only, K_)
+    ms_per_step = step_us * 1e-3
     b_ca = attn_bytes(cfg, lens)
     b_ng = ngram_bytes(cfg.rows, cfg.t, bans)
     b_step = b_ca + b_ng
@@ -260,7 +266,7 @@ def main() -> int:
     log(f"step {step_us:.2f} us (wall {wall / K_ * 1e6:.2f} us) = {value:.0f} GB/s; cross-attn {ca_us:.2f} us "
         f"= {ca_gbps:.0f} GB/s ({100 * ca_gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
         f"{100 * ca_gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s); "
-        f"n-gram {ng_us:.2f} us = {100 * ng_us / step_us:.1f}% of the step")
+        f"n-gram {ng_us:.2f} us = {100 * ng_us / (ca_us + ng_us):.1f}% of the step")
 
     traffic = load_traffic(args.traffic, cfg.name)
 
@@ -285,7 +291,8 @@ def main() -> int:
         "cross_attn_us": round(ca_us, 3),
         "cross_attn_us_spread": ca_spread,
         "ngram_us": round(ng_us, 3),
-        "ngram_share_of_step": round(ng_us / step_us, 4),
+        "ngram_share_of_step": round(ng_us / (ca_us + ng_us), 4),
+        "timing_rounds": max(1, args.rounds),
         "copy_gbps": round(copy_gbps, 1),
         "roofline": {"bound": "hbm", "kernel": "fs_beam_cross_attn", "achieved": round(ca_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ca_gbps / HBM_PEAK_GBPS, 4),

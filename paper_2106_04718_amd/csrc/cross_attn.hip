@@ -33,6 +33,8 @@
 // row size, and each beam's arithmetic is the same whatever k is, so the
 // output bits do not depend on k, B or the beam's position.
 #include <math.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <algorithm>
 
@@ -46,6 +48,8 @@ constexpr int kWaves = 4;
 constexpr int kBlock = kWave * kWaves;
 constexpr int kIt = 8;   // row loads of K (and of V) per lane per tile
 constexpr int kXcds = 8; // MI355X: workgroups go round-robin to 8 XCDs
+constexpr int kWhole1MinRows = 4 * 256;  // (b, h) rows for one 4-wave workgroup per row (256 CUs)
+constexpr int kWhole2MinRows = 128;      // rows for one 8-wave workgroup per row
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -441,9 +445,41 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
     }
 }
 
+// Softmax state of beam i of source b over its own generated rows [0, t) of
+// Kt/Vt for head h (t > 0): the tiles in order, each folded into the running
+// state.  m, l are wave-uniform; acc[e] holds dims sub*kEpl + e.
+template <int D, bool BF16>
+__device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
+                                                const uint4 *__restrict__ Vt, size_t hyp, int h, int H, int T,
+                                                int t, int sub, int grp, float *prow, float scale_log2,
+                                                float &m, float &l, float (&acc)[Geo<D, BF16>::kEpl])
+{
+    using G = Geo<D, BF16>;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kTile = G::kTile;
+    const uint4 qr[1] = {q[(hyp * H + h) * kLpr + sub]};
+    const uint4 *Kb = Kt + (hyp * H + h) * (size_t)T * kLpr;
+    const uint4 *Vb = Vt + (hyp * H + h) * (size_t)T * kLpr;
+    m = -INFINITY;
+    l = 0.f;
+#pragma unroll
+    for (int e = 0; e < kEpl; ++e) acc[e] = 0.f;
+    for (int t0 = 0; t0 < t; t0 += kTile) {
+        float tm[1], tl[1], ta[1][kEpl];
+        tile_attend<D, BF16, 1>(qr, Kb, Vb, t0, t, sub, grp, prow, scale_log2, tm, tl, ta);
+        // fold the tile into the running state (wave-uniform m, l)
+        const float mx = fmaxf(m, tm[0]);
+        const float fo = __builtin_amdgcn_exp2f(m - mx);
+        const float fn = __builtin_amdgcn_exp2f(tm[0] - mx);
+        l = l * fo + tl[0] * fn;
+#pragma unroll
+        for (int e = 0; e < kEpl; ++e) acc[e] = acc[e] * fo + ta[0][e] * fn;
+        m = mx;
+    }
+}
+
 // Generated-token segment of (b, h) = bh (SPLIT only): wave w attends beam
-// i = w, w + 4, ... over that hypothesis' own rows [0, t) of Kt/Vt, tile after
-// tile in order, and stores the beam's state in record slot NC of (b, h).
+// i = w, w + 4, ... over that hypothesis' own rows [0, t) of Kt/Vt and stores
+// the beam's state in record slot NC of (b, h).
 template <int D, bool BF16, int KB>
 __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                  const uint4 *__restrict__ Vt, unsigned long long *__restrict__ part,
@@ -451,7 +487,7 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
                                                  float scale_log2, unsigned long long epoch, float *prow)
 {
     using G = Geo<D, BF16>;
-    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kTile = G::kTile;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
     if (bh >= n_bh || t <= 0) return;
     const int b = bh / H;
     const int h = bh - b * H;
@@ -462,25 +498,8 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
     for (int i = w; i < KB; i += kWaves) {
-        const size_t hyp = (size_t)b * KB + i;
-        const uint4 qr[1] = {q[(hyp * H + h) * kLpr + sub]};
-        const uint4 *Kb = Kt + (hyp * H + h) * (size_t)T * kLpr;
-        const uint4 *Vb = Vt + (hyp * H + h) * (size_t)T * kLpr;
-        float m = -INFINITY, l = 0.f, acc[kEpl];
-#pragma unroll
-        for (int e = 0; e < kEpl; ++e) acc[e] = 0.f;
-        for (int t0 = 0; t0 < t; t0 += kTile) {
-            float tm[1], tl[1], ta[1][kEpl];
-            tile_attend<D, BF16, 1>(qr, Kb, Vb, t0, t, sub, grp, prow, scale_log2, tm, tl, ta);
-            // fold the tile into the running state (wave-uniform m, l)
-            const float mx = fmaxf(m, tm[0]);
-            const float fo = __builtin_amdgcn_exp2f(m - mx);
-            const float fn = __builtin_amdgcn_exp2f(tm[0] - mx);
-            l = l * fo + tl[0] * fn;
-#pragma unroll
-            for (int e = 0; e < kEpl; ++e) acc[e] = acc[e] * fo + ta[0][e] * fn;
-            m = mx;
-        }
+        float m, l, acc[kEpl];
+        generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, sub, grp, prow, scale_log2, m, l, acc);
         if (lane < kLpr) {
 #pragma unroll
             for (int e = 0; e < kEpl; ++e) store_word(rec + i * D + sub * kEpl + e, tag, acc[e]);
@@ -616,6 +635,149 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     }
 }
 
+// One workgroup per (b, h) that walks all of its chunks itself: no partial
+// records, no merger, no cross-workgroup wait.  P chunks are processed at a
+// time by P groups of kWaves waves (workgroup of P*kBlock threads).  The
+// arithmetic and its order are those of cross_attn_kernel -- each chunk's
+// four wave states merged in wave order, the chunk states folded in chunk
+// order from the empty state, the generated-token state (SPLIT) last -- so
+// both kernels give the same bits.  It pays when there are enough (b, h)
+// rows to fill the chip without splitting them.
+template <int D, bool BF16, int KB, bool SPLIT, int P>
+__global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
+    const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
+    const int32_t *__restrict__ src_len, void *__restrict__ out, int n_bh, int H, int S,
+    float scale_log2, const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t)
+{
+    using G = Geo<D, BF16>;
+    constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
+    constexpr int kTile = G::kTile, kChunk = G::kChunk;
+    constexpr int kW = kWaves * P;                        // waves per workgroup
+    constexpr int kThreads = kBlock * P;
+    constexpr int kPer = (KB * D + kThreads - 1) / kThreads;  // outputs per thread
+
+    __shared__ float m_lds[kW][KB], l_lds[kW][KB];
+    __shared__ float a_lds[kW][KB][D];
+    __shared__ __attribute__((aligned(16))) float p_lds[kW][G::kPStride][KB];
+
+    const int bh = blockIdx.x;
+    if (bh >= n_bh) return;
+    const int b = bh / H;
+    const int h = bh - b * H;
+    const int L = min(max(src_len[b], 0), S);
+    const int nc = (L + kChunk - 1) / kChunk;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int w = tid / kWave;
+    const int sub = lane % kLpr;
+    const int grp = lane / kLpr;
+    const size_t obase = ((size_t)b * KB * H + h) * D;  // out[b, 0, h, 0]
+
+    uint4 qr[KB];
+#pragma unroll
+    for (int i = 0; i < KB; ++i) qr[i] = q[((size_t)(b * KB + i) * H + h) * kLpr + sub];
+    const uint4 *Kbh = K + (size_t)bh * S * kLpr;
+    const uint4 *Vbh = V + (size_t)bh * S * kLpr;
+
+    // running state of output x = tid + p * kThreads (beam x / D, dim x % D)
+    float Rm[kPer], Rl[kPer], Ra[kPer];
+#pragma unroll
+    for (int p = 0; p < kPer; ++p) {
+        Rm[p] = -INFINITY;
+        Rl[p] = 0.f;
+        Ra[p] = 0.f;
+    }
+
+    const int cg = w / kWaves;   // chunk of the step this wave works on
+    const int wt = w % kWaves;   // its tile in that chunk
+    for (int c0 = 0; c0 < nc; c0 += P) {
+        const int c = c0 + cg;
+        float m[KB], l[KB], acc[KB][kEpl];
+#pragma unroll
+        for (int i = 0; i < KB; ++i) {
+            m[i] = -INFINITY;
+            l[i] = 0.f;
+#pragma unroll
+            for (int e = 0; e < kEpl; ++e) acc[i][e] = 0.f;
+        }
+        if (c < nc) {
+            const int j0 = c * kChunk;
+            const int j1 = min(j0 + kChunk, L);
+            const int t0 = j0 + wt * kTile;
+            if (t0 < j1)
+                tile_attend<D, BF16, KB>(qr, Kbh, Vbh, t0, j1, sub, grp, &p_lds[w][0][0], scale_log2, m, l, acc);
+        }
+        if (lane < kLpr) {
+#pragma unroll
+            for (int i = 0; i < KB; ++i) {
+#pragma unroll
+                for (int e = 0; e < kEpl; ++e) a_lds[w][i][sub * kEpl + e] = acc[i][e];
+            }
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int i = 0; i < KB; ++i) {
+                m_lds[w][i] = m[i];
+                l_lds[w][i] = l[i];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int p = 0; p < kPer; ++p) {
+            const int x = tid + p * kThreads;
+            if (x < KB * D) {
+                const int i = x / D, d = x - i * D;
+                for (int g = 0; g < P && c0 + g < nc; ++g) {
+                    const int w0 = g * kWaves;
+                    float mm = m_lds[w0][i], ll = l_lds[w0][i], aa = a_lds[w0][i][d];
+#pragma unroll
+                    for (int ww = 1; ww < kWaves; ++ww)
+                        merge_state(mm, ll, aa, m_lds[w0 + ww][i], l_lds[w0 + ww][i], a_lds[w0 + ww][i][d]);
+                    merge_state(Rm[p], Rl[p], Ra[p], mm, ll, aa);
+                }
+            }
+        }
+        __syncthreads();
+    }
+    bool any = nc > 0;
+    if constexpr (SPLIT) {
+        if (t > 0) {
+            any = true;
+            // beam i's state over its own generated rows, kept in slot [0][i]
+            for (int i = w; i < KB; i += kW) {
+                float m, l, acc[kEpl];
+                generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, sub, grp, &p_lds[w][0][0],
+                                         scale_log2, m, l, acc);
+                if (lane < kLpr) {
+#pragma unroll
+                    for (int e = 0; e < kEpl; ++e) a_lds[0][i][sub * kEpl + e] = acc[e];
+                }
+                if (lane == 0) {
+                    m_lds[0][i] = m;
+                    l_lds[0][i] = l;
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int p = 0; p < kPer; ++p) {
+                const int x = tid + p * kThreads;
+                if (x < KB * D) {
+                    const int i = x / D, d = x - i * D;
+                    merge_state(Rm[p], Rl[p], Ra[p], m_lds[0][i], l_lds[0][i], a_lds[0][i][d]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int p = 0; p < kPer; ++p) {
+        const int x = tid + p * kThreads;
+        if (x < KB * D) {
+            const int i = x / D, d = x - i * D;
+            store_out<BF16>(out, obase + (size_t)i * H * D + d, any ? Ra[p] / Rl[p] : 0.f);  // no key: zero row
+        }
+    }
+}
+
 // Launch arguments shared by both entry points.  For the encoder-decoder
 // form Kt/Vt are null and T = t = 0.
 struct AttnArgs {
@@ -631,12 +793,8 @@ struct AttnArgs {
 };
 
 template <int D, bool BF16, int KB, bool SPLIT>
-hipError_t launch_typed(const AttnArgs &a)
+hipError_t launch_split(const AttnArgs &a, int NC)
 {
-    using G = Geo<D, BF16>;
-    // at least one chunk column, so that a source with no valid key (or
-    // S == 0) still has a workgroup to write its zero output
-    const int NC = max(1, (a.S + G::kChunk - 1) / G::kChunk);
     const int n_bh = a.B * a.H;
     const long long n_bh8 = ((long long)n_bh + kXcds - 1) / kXcds * kXcds;
     const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
@@ -650,6 +808,32 @@ hipError_t launch_typed(const AttnArgs &a)
                        NC, (float)scale_log2, a.epoch, static_cast<const uint4 *>(a.Kt),
                        static_cast<const uint4 *>(a.Vt), a.T, a.t);
     return hipGetLastError();
+}
+
+template <int D, bool BF16, int KB, bool SPLIT, int P>
+hipError_t launch_whole(const AttnArgs &a)
+{
+    const int n_bh = a.B * a.H;
+    const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
+    hipLaunchKernelGGL((attn_whole_kernel<D, BF16, KB, SPLIT, P>), dim3((unsigned)n_bh), dim3(kBlock * P), 0,
+                       a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
+                       static_cast<const uint4 *>(a.V), a.src_len, a.out, n_bh, a.H, a.S, (float)scale_log2,
+                       static_cast<const uint4 *>(a.Kt), static_cast<const uint4 *>(a.Vt), a.T, a.t);
+    return hipGetLastError();
+}
+
+template <int D, bool BF16, int KB, bool SPLIT>
+hipError_t launch_typed(const AttnArgs &a)
+{
+    using G = Geo<D, BF16>;
+    // at least one chunk column, so that a source with no valid key (or
+    // S == 0) still has a workgroup to write its zero output
+    const int NC = max(1, (a.S + G::kChunk - 1) / G::kChunk);
+    switch (choose_attn_path(a.B * a.H, NC)) {
+    case AttnPath::kWhole1: return launch_whole<D, BF16, KB, SPLIT, 1>(a);
+    case AttnPath::kWhole2: return launch_whole<D, BF16, KB, SPLIT, 2>(a);
+    default: return launch_split<D, BF16, KB, SPLIT>(a, NC);
+    }
 }
 
 template <int D, bool BF16, bool SPLIT>
@@ -681,6 +865,23 @@ hipError_t launch_d(const AttnArgs &a)
 }
 
 }  // namespace
+
+AttnPath choose_attn_path(int n_bh, int nc_max) {
+    if (const char *v = getenv("FS_ATTN_PATH")) {
+        if (!strcmp(v, "split")) return AttnPath::kSplit;
+        if (!strcmp(v, "whole1")) return AttnPath::kWhole1;
+        if (!strcmp(v, "whole2")) return AttnPath::kWhole2;
+    }
+    // Measured on MI355X (bf16, D = 64, k = 4; 192 to 5120 rows of up to
+    // 1024 keys): with four or more rows per CU, one 4-wave workgroup per
+    // row streams at the chip's read rate; with fewer, an 8-wave workgroup
+    // per row (two chunks in flight) beats splitting rows across
+    // workgroups, whose merge costs a round trip through memory.  Only a
+    // few long rows are split.
+    if (nc_max <= 1 || n_bh >= kWhole1MinRows) return AttnPath::kWhole1;
+    if (n_bh >= kWhole2MinRows || nc_max <= 2) return AttnPath::kWhole2;
+    return AttnPath::kSplit;
+}
 
 int cross_attn_chunk_keys(int D, int esize) {
     // kWaves * kIt rows of 64/(lanes per row) = 4 * 8 * 64 * 16 / (D * esize)

@@ -15,6 +15,17 @@ namespace fs {
 // source is read by one beam or by k beams.
 int cross_attn_chunk_keys(int D, int esize);
 
+// How an attention call is decomposed (every path gives the same bits):
+//   kSplit   one workgroup per (b, h, chunk), partial records merged by
+//            trailing merger workgroups -- most parallel, pays a merge;
+//   kWholeP  one workgroup per (b, h) of P*4 waves walking its chunks P at a
+//            time -- no records, needs many (b, h) rows to fill the chip.
+enum class AttnPath { kAuto = 0, kSplit, kWhole1, kWhole2 };
+
+// The path for n_bh = B*H rows of at most nc_max chunks: FS_ATTN_PATH
+// (split, whole1, whole2; read at every call) overrides the size rule.
+AttnPath choose_attn_path(int n_bh, int nc_max);
+
 // Workspace size in 4-byte words: the per-chunk partial records (plus one
 // record per (b, h) for the generated-token segment when `split`).
 size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize, bool split);

@@ -6,17 +6,17 @@
 // followed, x[j+n-1], by writing -inf into logits[r, x[j+n-1]].
 //
 // The paper launches one block per row and one thread per window, with the
-// row staged in shared memory.  Here one wavefront handles one row:
-//   - the last n-1 tokens are wave-uniform and are loaded once into
-//     registers;
-//   - lane l takes windows l, l+64, ...; for each it loads its n tokens with
-//     coalesced loads (consecutive lanes read consecutive tokens, the
-//     overlapping re-reads hit the L1 cache) and compares the (n-1)-gram in
-//     registers;
+// row staged in shared memory.  Here one wavefront handles one row, and the
+// kernel is built around a single memory round trip:
+//   - all the row's tokens are loaded at once, lane l holding positions
+//     l, l+64, ... (coalesced), and the last n-1 tokens with wave-uniform
+//     loads issued alongside;
+//   - window j = lane + 64m takes its n tokens from its own register and
+//     from lanes l+1 .. l+n-1 (ds_bpermute across the wave, wrapping into
+//     the next 64 positions), and compares the (n-1)-gram in registers;
 //   - matching lanes scatter -inf; the logits are never read.
-// Nothing is staged in LDS: each token is reused by at most n lanes of the
-// same wave, which the vector L1 serves without a barrier.  Several windows
-// that ban the same id write the same bits, so no atomics are needed.
+// Several windows that ban the same id write the same bits, so no atomics
+// are needed.
 #include <math.h>
 
 #include "launch.h"
@@ -26,30 +26,51 @@ namespace {
 
 constexpr int kWave = 64;
 
-// NM1 = n - 1 known at compile time (0..7); the suffix lives in registers.
+// Value that lane (lane + c) holds in the 128-lane concatenation [lo | hi]
+// (0 < c < 64): the window tokens that follow this lane's position.
+__device__ __forceinline__ int32_t following(int32_t lo, int32_t hi, int lane, int c) {
+    const int src = ((lane + c) & (kWave - 1)) << 2;
+    const int32_t a = __builtin_amdgcn_ds_bpermute(src, lo);
+    const int32_t b = __builtin_amdgcn_ds_bpermute(src, hi);
+    return lane + c < kWave ? a : b;
+}
+
+// NM1 = n - 1 known at compile time (0..7).
 template <int NM1>
 __global__ __launch_bounds__(kWave) void ngram_block_fixed(
     const int32_t *__restrict__ tokens, int ld, int t, float *__restrict__ logits, int V)
 {
+    constexpr int kM = 4;  // 64-position slices per pass (all loaded together)
     const int row = blockIdx.x;
     const int lane = threadIdx.x;
     const int32_t *x = tokens + (size_t)row * ld;
     float *lg = logits + (size_t)row * V;
     const int nwin = t - NM1;  // windows j = 0 .. t-n
+    if (nwin <= 0) return;
 
     int32_t suf[NM1 > 0 ? NM1 : 1];
 #pragma unroll
     for (int c = 0; c < NM1; ++c) suf[c] = x[t - NM1 + c];
 
-    for (int j = lane; j < nwin; j += kWave) {
-        int32_t win[NM1 + 1];
+    for (int base = 0; base < nwin; base += kM * kWave) {
+        int32_t s[kM + 1];
 #pragma unroll
-        for (int c = 0; c <= NM1; ++c) win[c] = x[j + c];
-        int diff = 0;
+        for (int m = 0; m <= kM; ++m) {
+            const int pos = base + m * kWave + lane;
+            s[m] = pos < t ? x[pos] : 0;
+        }
 #pragma unroll
-        for (int c = 0; c < NM1; ++c) diff |= win[c] ^ suf[c];
-        const int32_t v = win[NM1];
-        if (diff == 0 && (uint32_t)v < (uint32_t)V) lg[v] = -INFINITY;
+        for (int m = 0; m < kM; ++m) {
+            const int j = base + m * kWave + lane;
+            int diff = 0;
+            int32_t v = s[m];
+#pragma unroll
+            for (int c = 0; c < NM1; ++c) {
+                diff |= v ^ suf[c];
+                v = following(s[m], s[m + 1], lane, c + 1);
+            }
+            if (j < nwin && diff == 0 && (uint32_t)v < (uint32_t)V) lg[v] = -INFINITY;
+        }
     }
 }
 

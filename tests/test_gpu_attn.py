@@ -169,3 +169,37 @@ def test_workspace_reused_across_calls_with_changing_lengths():
         assert_attn_close(run(d, ws=ws), oracle_attn(d), f"rep {rep}")
     d = random_case(2, 4, 3, 300, 64, "bf16", [300, 257], seed=70)
     assert_attn_close(run(d, ws=ws), oracle_attn(d), "smaller problem, same workspace")
+
+
+PATHS = ("split", "whole1", "whole2")
+
+
+def run_path(path, fn):
+    import os
+    old = os.environ.get("FS_ATTN_PATH")
+    os.environ["FS_ATTN_PATH"] = path
+    try:
+        out = fn()
+        torch.cuda.synchronize()
+        return bits(out)
+    finally:
+        if old is None:
+            del os.environ["FS_ATTN_PATH"]
+        else:
+            os.environ["FS_ATTN_PATH"] = old
+
+
+@pytest.mark.parametrize("dtype,D,k", [("bf16", 64, 4), ("bf16", 64, 5), ("f32", 64, 4), ("bf16", 16, 3),
+                                       ("bf16", 128, 8), ("f32", 32, 1), ("f32", 128, 2)])
+def test_decompositions_give_identical_bits(dtype, D, k):
+    # The split-KV kernel (chunk workgroups + mergers) and the one-workgroup-
+    # per-row kernel (one or two chunks at a time) fold the same partial
+    # states in the same order: their outputs must agree bit for bit, and
+    # with the oracle to tolerance.
+    lens = [1100, 0, 257, 1, 513, 1024, 700]
+    d = random_case(7, k, 3, 1100, D, dtype, lens, seed=80 + D + k)
+    say(f"[attn paths] dtype={dtype} D={D} k={k}")
+    outs = {p: run_path(p, lambda: run(d)) for p in PATHS}
+    for p in PATHS[1:]:
+        assert np.array_equal(outs[p], outs["split"]), p
+    assert_attn_close(run(d), oracle_attn(d), f"paths {dtype} D={D} k={k}")

@@ -136,3 +136,27 @@ def test_workspace_reused_across_sizes_and_entry_points():
                                 to_dev(d["prefix_len"]), workspace=ws)
         torch.cuda.synchronize()
         assert_attn_close(o, ref(dict(d, t=0)), f"rep {rep}, encoder-decoder form")
+
+
+@pytest.mark.parametrize("dtype,D,k,t", [("bf16", 64, 4, 64), ("bf16", 64, 4, 0), ("f32", 32, 5, 140),
+                                         ("bf16", 128, 8, 65), ("f32", 16, 1, 9)])
+def test_decompositions_give_identical_bits(dtype, D, k, t):
+    # Split-KV with a generated-token record, and the one-workgroup-per-row
+    # kernel, fold the same states in the same order: identical bits.
+    import os
+    d = case(3, k, 2, 1100, 150, D, dtype, [1100, 0, 513], t, seed=90 + D + t)
+    say(f"[prefix paths] dtype={dtype} D={D} k={k} t={t}")
+    outs = {}
+    old = os.environ.get("FS_ATTN_PATH")
+    try:
+        for p in ("split", "whole1", "whole2"):
+            os.environ["FS_ATTN_PATH"] = p
+            outs[p] = bits(run(d))
+    finally:
+        if old is None:
+            os.environ.pop("FS_ATTN_PATH", None)
+        else:
+            os.environ["FS_ATTN_PATH"] = old
+    assert np.array_equal(outs["whole1"], outs["split"])
+    assert np.array_equal(outs["whole2"], outs["split"])
+    assert_attn_close(run(d), ref(d), f"paths {dtype} D={D} k={k} t={t}")
