@@ -37,6 +37,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "launch.h"
 
@@ -370,6 +371,347 @@ __device__ __forceinline__ void store_word(unsigned long long *p, unsigned long 
     __hip_atomic_store(p, tag | __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+
+// ---- tile policies -----------------------------------------------------------
+// A policy attends one wave tile of keys and keeps one wave's softmax state
+// per beam.  The kernels below only move these states through LDS and the
+// workspace, so every decomposition of a call folds the same tile states in
+// the same order.
+//   ValuTile  fp32, and bf16 with D = 16: the VALU routine above.
+//   MfmaTile  bf16 with D >= 32: both contractions on the matrix cores.
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+template <int D, bool BF16, int KB>
+struct ValuTile {
+    using G = Geo<D, BF16>;
+    static constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
+    static constexpr int kLdsBytes = G::kPStride * KB * 4;  // per wave
+    struct Q { uint4 r[KB]; };
+    // m, l wave-uniform; acc[i][e] holds dims sub*kEpl + e in every lane
+    struct St { float m[KB], l[KB], acc[KB][kEpl]; };
+
+    // queries of hypotheses hyp0 .. hyp0 + KB - 1, head h
+    static __device__ __forceinline__ void load_q(Q &q, const uint4 *__restrict__ qp, size_t hyp0, int h, int H,
+                                                  int lane) {
+        const int sub = lane % kLpr;
+#pragma unroll
+        for (int i = 0; i < KB; ++i) q.r[i] = qp[((hyp0 + i) * H + h) * kLpr + sub];
+    }
+    static __device__ __forceinline__ void init(St &s) {
+#pragma unroll
+        for (int i = 0; i < KB; ++i) {
+            s.m[i] = -INFINITY;
+            s.l[i] = 0.f;
+#pragma unroll
+            for (int e = 0; e < kEpl; ++e) s.acc[i][e] = 0.f;
+        }
+    }
+    static __device__ __forceinline__ void attend(const Q &q, const uint4 *__restrict__ Kb,
+                                                  const uint4 *__restrict__ Vb, int t0, int j1, int lane,
+                                                  void *lds, float scale_log2, St &s) {
+        tile_attend<D, BF16, KB>(q.r, Kb, Vb, t0, j1, lane % kLpr, lane / kLpr, static_cast<float *>(lds),
+                                 scale_log2, s.m, s.l, s.acc);
+    }
+    // fold the state of a later tile into the running state
+    static __device__ __forceinline__ void fold(St &s, const St &t) {
+#pragma unroll
+        for (int i = 0; i < KB; ++i) {
+            const float mx = fmaxf(s.m[i], t.m[i]);
+            const float fo = __builtin_amdgcn_exp2f(s.m[i] - mx);
+            const float fn = __builtin_amdgcn_exp2f(t.m[i] - mx);
+            s.l[i] = s.l[i] * fo + t.l[i] * fn;
+#pragma unroll
+            for (int e = 0; e < kEpl; ++e) s.acc[i][e] = s.acc[i][e] * fo + t.acc[i][e] * fn;
+            s.m[i] = mx;
+        }
+    }
+    // this wave's state into LDS: m_w[KB], l_w[KB], a_w[KB][D]
+    static __device__ __forceinline__ void to_lds(const St &s, int lane, float *m_w, float *l_w, float *a_w) {
+        if (lane < kLpr) {
+#pragma unroll
+            for (int i = 0; i < KB; ++i) {
+#pragma unroll
+                for (int e = 0; e < kEpl; ++e) a_w[i * D + lane * kEpl + e] = s.acc[i][e];
+            }
+        }
+        if (lane == 0) {
+#pragma unroll
+            for (int i = 0; i < KB; ++i) {
+                m_w[i] = s.m[i];
+                l_w[i] = s.l[i];
+            }
+        }
+    }
+    // beam 0's state as tagged record words: acc[D] at acc_w, then m, l
+    static __device__ __forceinline__ void to_record(const St &s, int lane, unsigned long long *acc_w,
+                                                     unsigned long long *m_w, unsigned long long *l_w,
+                                                     unsigned long long tag);
+};
+
+// Value of x in lanes l & ~MASK and l | MASK (MASK = 16 or 32), in that
+// order, in both lanes: combining the pair commutes nothing, so both lanes
+// get bit-identical results.
+template <int MASK>
+__device__ __forceinline__ void lane_pair(float x, float &lo, float &hi) {
+    const unsigned u = __float_as_uint(x);
+    if constexpr (MASK == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        lo = __uint_as_float(r[0]);
+        hi = __uint_as_float(r[1]);
+    } else {
+        const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+        lo = __uint_as_float(r[0]);
+        hi = __uint_as_float(r[1]);
+    }
+}
+// max / sum over the four lanes n, n + 16, n + 32, n + 48 of a column
+__device__ __forceinline__ float col_max(float x) {
+    float a, b;
+    lane_pair<16>(x, a, b);
+    x = fmaxf(a, b);
+    lane_pair<32>(x, a, b);
+    return fmaxf(a, b);
+}
+__device__ __forceinline__ float col_sum(float x) {
+    float a, b;
+    lane_pair<16>(x, a, b);
+    x = a + b;
+    lane_pair<32>(x, a, b);
+    return a + b;
+}
+
+// bf16 tile on the matrix cores (v_mfma_f32_16x16x32_bf16; D = 32, 64, 128).
+// The tile has T = 4096 / D keys (the row-load geometry of the VALU
+// routine, so chunks are the same size).  K and V rows are loaded whole
+// and coalesced, then pass through one swizzled LDS tile per wave (K first,
+// then V in its place) to reach the operand layouts.  Lane l = 16 g + n:
+//   QK^T  S^T[key][beam] = K[key][:] . q[beam][:]: the A operand is K
+//         (lane: key 16 kb + n, 16 bytes at dim 32 s + 8 g), the B operand
+//         the queries (column n = beam n < KB, the other columns zero).
+//         Lane l gets the scores of beam n for keys 16 kb + 4 g + i.
+//   softmax  per lane over its 4 NKB scores, then over the four lanes of
+//         its column: every beam at once, no LDS.
+//   PV    O^T[dim][beam] = V^T[dim][key] . P^T[key][beam].  P^T is the B
+//         operand straight from the score registers (rounded to bf16; the
+//         sum uses the rounded weights, so they add up to one).  V^T comes
+//         from the tile's V rows staged in LDS and read back with
+//         ds_read_b64_tr_b16, which transposes 16-bit elements within each
+//         group of 16 lanes.  Lane l gets dims 16 mb + 4 g + i of beam n.
+template <int D, int KB>
+struct MfmaTile {
+    static constexpr int T = 4096 / D;    // keys per tile
+    static constexpr int NKB = T / 16;    // 16-key blocks
+    static constexpr int NS = D / 32;     // 32-dim steps of QK^T
+    static constexpr int NU = D / 16;     // 32-byte units per row = 16-dim output blocks
+    static constexpr int kLpr = D / 8;    // 16-byte slices per row
+    static constexpr int kLdsBytes = T * D * 2;  // one tile of rows (8 KB): K, then V
+    static_assert(D == 32 || D == 64 || D == 128, "MFMA tile needs D in {32, 64, 128}");
+    static_assert(KB <= 16, "beams are the 16 columns of the MFMA");
+    static_assert(NKB % 2 == 0, "PV takes 32 keys per instruction");
+    struct Q { bf16x8_t b[NS]; };
+    // column state of beam n = lane & 15: m, l identical in the column's
+    // four lanes; acc[mb][i] holds dim 16 mb + 4 (lane >> 4) + i
+    struct St { float m, l; f32x4_t acc[NU]; };
+
+    // 32-byte unit of row r holding unit c: a XOR swizzle that spreads the
+    // 16 rows of one transposed read over all LDS banks
+    static __device__ __forceinline__ int unit(int r, int c) {
+        constexpr int sh = NU == 2 ? 2 : NU == 4 ? 1 : 0;
+        return c ^ ((r >> sh) & (NU - 1));
+    }
+    static __device__ __forceinline__ void load_q(Q &q, const uint4 *__restrict__ qp, size_t hyp0, int h, int H,
+                                                  int lane) {
+        const int n = lane & 15, g = lane >> 4;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (n < KB) v = qp[((hyp0 + n) * H + h) * kLpr + 4 * s + g];
+            q.b[s] = __builtin_bit_cast(bf16x8_t, v);
+        }
+    }
+    static __device__ __forceinline__ void init(St &s) {
+        s.m = -INFINITY;
+        s.l = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < NU; ++mb) s.acc[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    // row r of the tile (2 D bytes), 16-byte slice sl, in the swizzled LDS tile
+    static __device__ __forceinline__ int lds_off(int r, int sl) {
+        return r * (2 * D) + (unit(r, sl >> 1) << 5) + ((sl & 1) << 4);
+    }
+    static __device__ __forceinline__ void lds_fence() {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    static __device__ __forceinline__ void attend(const Q &q, const uint4 *__restrict__ Kb,
+                                                  const uint4 *__restrict__ Vb, int t0, int j1, int lane,
+                                                  void *lds, float scale_log2, St &st) {
+        const int n = lane & 15, g = lane >> 4;
+        // Row loads in the coalesced layout: kLpr lanes per row, so one
+        // instruction reads whole rows (loads of 16 half rows each are
+        // markedly slower).  Rows past j1 re-read row j1 - 1 and are masked.
+        // All K first, so its trip through LDS can start while V is in flight.
+        constexpr int kRpi = kWave / kLpr;
+        const int sub = lane % kLpr, grp = lane / kLpr;
+        uint4 kr[kIt], vr[kIt];
+#pragma unroll
+        for (int u = 0; u < kIt; ++u) kr[u] = load_nt(Kb + (size_t)min(t0 + u * kRpi + grp, j1 - 1) * kLpr + sub);
+#pragma unroll
+        for (int u = 0; u < kIt; ++u) vr[u] = load_nt(Vb + (size_t)min(t0 + u * kRpi + grp, j1 - 1) * kLpr + sub);
+        // K through LDS into the MFMA A layout: lane l takes row 16 kb + n,
+        // dims 32 s + 8 g .. + 8
+        char *vt = static_cast<char *>(lds);
+#pragma unroll
+        for (int u = 0; u < kIt; ++u) *reinterpret_cast<uint4 *>(vt + lds_off(u * kRpi + grp, sub)) = kr[u];
+        lds_fence();
+        uint4 ka[NKB][NS];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) ka[kb][s] = *reinterpret_cast<const uint4 *>(vt + lds_off(16 * kb + n, 4 * s + g));
+        }
+        lds_fence();
+        // the V rows take the K rows' place (this wave's reads of K are done:
+        // LDS instructions of one wave complete in order)
+#pragma unroll
+        for (int u = 0; u < kIt; ++u) *reinterpret_cast<uint4 *>(vt + lds_off(u * kRpi + grp, sub)) = vr[u];
+        f32x4_t sc[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ka[kb][s]), q.b[s],
+                                                                 sc[kb], 0, 0, 0);
+        }
+        // scores in the base-2 domain; keys past j1 get weight zero
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const bool ok = t0 + 16 * kb + 4 * g + i < j1;
+                sc[kb][i] = ok ? sc[kb][i] * scale_log2 : -INFINITY;
+                mx = fmaxf(mx, sc[kb][i]);
+            }
+        }
+        mx = col_max(mx);  // finite: key t0 is valid
+        bf16x8_t pb[NKB / 2];
+        float ls = 0.f;
+#pragma unroll
+        for (int pp = 0; pp < NKB / 2; ++pp) {
+            f32x8_t e;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                e[i] = __builtin_amdgcn_exp2f(sc[2 * pp][i] - mx);
+                e[4 + i] = __builtin_amdgcn_exp2f(sc[2 * pp + 1][i] - mx);
+            }
+            pb[pp] = __builtin_convertvector(e, bf16x8_t);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) ls += (float)pb[pp][i];
+        }
+        ls = col_sum(ls);
+        lds_fence();
+        // PV: MFMA pp contracts over keys [32 pp, 32 pp + 32) in the order
+        // the score registers hold them: k = 8 g + j stands for key
+        // 16 (2 pp + j / 4) + 4 g + j % 4.
+        f32x4_t o[NU];
+#pragma unroll
+        for (int mb = 0; mb < NU; ++mb) o[mb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int pp = 0; pp < NKB / 2; ++pp) {
+#pragma unroll
+            for (int mb = 0; mb < NU; ++mb) {
+                i16x4_t t[2];
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int row = 32 * pp + 16 * r + 4 * g + (n >> 2);
+                    const int off = row * (2 * D) + (unit(row, mb) << 5) + ((n & 3) << 3);
+                    t[r] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) i16x4_t *)(vt + off));
+                }
+                const auto a = __builtin_shufflevector(t[0], t[1], 0, 1, 2, 3, 4, 5, 6, 7);
+                o[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), pb[pp], o[mb],
+                                                                0, 0, 0);
+            }
+        }
+        // keep the next tile's LDS writes behind this tile's reads
+        lds_fence();
+        st.m = mx;
+        st.l = ls;
+#pragma unroll
+        for (int mb = 0; mb < NU; ++mb) st.acc[mb] = o[mb];
+    }
+    static __device__ __forceinline__ void fold(St &s, const St &t) {
+        const float mx = fmaxf(s.m, t.m);
+        const float fo = __builtin_amdgcn_exp2f(s.m - mx);
+        const float fn = __builtin_amdgcn_exp2f(t.m - mx);
+        s.l = s.l * fo + t.l * fn;
+#pragma unroll
+        for (int mb = 0; mb < NU; ++mb) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s.acc[mb][i] = s.acc[mb][i] * fo + t.acc[mb][i] * fn;
+        }
+        s.m = mx;
+    }
+    static __device__ __forceinline__ void to_lds(const St &s, int lane, float *m_w, float *l_w, float *a_w) {
+        const int n = lane & 15, g = lane >> 4;
+        if (n < KB) {
+#pragma unroll
+            for (int mb = 0; mb < NU; ++mb) *reinterpret_cast<f32x4_t *>(a_w + n * D + 16 * mb + 4 * g) = s.acc[mb];
+            if (g == 0) {
+                m_w[n] = s.m;
+                l_w[n] = s.l;
+            }
+        }
+    }
+    static __device__ __forceinline__ void to_record(const St &s, int lane, unsigned long long *acc_w,
+                                                     unsigned long long *m_w, unsigned long long *l_w,
+                                                     unsigned long long tag);
+};
+
+template <int D, bool BF16, int KB>
+using Tile = typename std::conditional<(BF16 && D >= 32), MfmaTile<D, KB>, ValuTile<D, BF16, KB>>::type;
+
+
+template <int D, bool BF16, int KB>
+__device__ __forceinline__ void ValuTile<D, BF16, KB>::to_record(const St &s, int lane, unsigned long long *acc_w,
+                                                                unsigned long long *m_w, unsigned long long *l_w,
+                                                                unsigned long long tag) {
+    if (lane < kLpr) {
+#pragma unroll
+        for (int e = 0; e < kEpl; ++e) store_word(acc_w + lane * kEpl + e, tag, s.acc[0][e]);
+    }
+    if (lane == 0) {
+        store_word(m_w, tag, s.m[0]);
+        store_word(l_w, tag, s.l[0]);
+    }
+}
+
+template <int D, int KB>
+__device__ __forceinline__ void MfmaTile<D, KB>::to_record(const St &s, int lane, unsigned long long *acc_w,
+                                                          unsigned long long *m_w, unsigned long long *l_w,
+                                                          unsigned long long tag) {
+    const int n = lane & 15, g = lane >> 4;
+    if (n == 0) {
+#pragma unroll
+        for (int mb = 0; mb < NU; ++mb) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) store_word(acc_w + 16 * mb + 4 * g + i, tag, s.acc[mb][i]);
+        }
+        if (g == 0) {
+            store_word(m_w, tag, s.m);
+            store_word(l_w, tag, s.l);
+        }
+    }
+}
+
+
 // Merger for (b, h) = bh: merges the chunk records of a source with more
 // than one chunk, in chunk order, and writes the normalised output.
 //
@@ -445,35 +787,26 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
     }
 }
 
-// Softmax state of beam i of source b over its own generated rows [0, t) of
+// Softmax state of hypothesis `hyp` over its own generated rows [0, t) of
 // Kt/Vt for head h (t > 0): the tiles in order, each folded into the running
-// state.  m, l are wave-uniform; acc[e] holds dims sub*kEpl + e.
+// state (beam slot 0 of a one-beam tile).
 template <int D, bool BF16>
 __device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                 const uint4 *__restrict__ Vt, size_t hyp, int h, int H, int T,
-                                                int t, int sub, int grp, float *prow, float scale_log2,
-                                                float &m, float &l, float (&acc)[Geo<D, BF16>::kEpl])
+                                                int t, int lane, void *lds, float scale_log2,
+                                                typename Tile<D, BF16, 1>::St &st)
 {
-    using G = Geo<D, BF16>;
-    constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kTile = G::kTile;
-    const uint4 qr[1] = {q[(hyp * H + h) * kLpr + sub]};
+    using TL = Tile<D, BF16, 1>;
+    constexpr int kLpr = Geo<D, BF16>::kLpr, kTile = Geo<D, BF16>::kTile;
+    typename TL::Q qv;
+    TL::load_q(qv, q, hyp, h, H, lane);
     const uint4 *Kb = Kt + (hyp * H + h) * (size_t)T * kLpr;
     const uint4 *Vb = Vt + (hyp * H + h) * (size_t)T * kLpr;
-    m = -INFINITY;
-    l = 0.f;
-#pragma unroll
-    for (int e = 0; e < kEpl; ++e) acc[e] = 0.f;
+    TL::init(st);
     for (int t0 = 0; t0 < t; t0 += kTile) {
-        float tm[1], tl[1], ta[1][kEpl];
-        tile_attend<D, BF16, 1>(qr, Kb, Vb, t0, t, sub, grp, prow, scale_log2, tm, tl, ta);
-        // fold the tile into the running state (wave-uniform m, l)
-        const float mx = fmaxf(m, tm[0]);
-        const float fo = __builtin_amdgcn_exp2f(m - mx);
-        const float fn = __builtin_amdgcn_exp2f(tm[0] - mx);
-        l = l * fo + tl[0] * fn;
-#pragma unroll
-        for (int e = 0; e < kEpl; ++e) acc[e] = acc[e] * fo + ta[0][e] * fn;
-        m = mx;
+        typename TL::St ts;
+        TL::attend(qv, Kb, Vb, t0, t, lane, lds, scale_log2, ts);
+        TL::fold(st, ts);
     }
 }
 
@@ -484,30 +817,21 @@ template <int D, bool BF16, int KB>
 __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                  const uint4 *__restrict__ Vt, unsigned long long *__restrict__ part,
                                                  int bh, int n_bh, int H, int NC, int T, int t,
-                                                 float scale_log2, unsigned long long epoch, float *prow)
+                                                 float scale_log2, unsigned long long epoch, void *lds)
 {
-    using G = Geo<D, BF16>;
-    constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
+    using TL = Tile<D, BF16, 1>;
     if (bh >= n_bh || t <= 0) return;
     const int b = bh / H;
     const int h = bh - b * H;
     const int lane = threadIdx.x & (kWave - 1);
     const int w = threadIdx.x / kWave;
-    const int sub = lane % kLpr, grp = lane / kLpr;
     constexpr int kRec = KB * (D + 2);
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
     for (int i = w; i < KB; i += kWaves) {
-        float m, l, acc[kEpl];
-        generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, sub, grp, prow, scale_log2, m, l, acc);
-        if (lane < kLpr) {
-#pragma unroll
-            for (int e = 0; e < kEpl; ++e) store_word(rec + i * D + sub * kEpl + e, tag, acc[e]);
-        }
-        if (lane == 0) {
-            store_word(rec + KB * D + i, tag, m);
-            store_word(rec + KB * D + KB + i, tag, l);
-        }
+        typename TL::St st;
+        generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, lds, scale_log2, st);
+        TL::to_record(st, lane, rec + i * D, rec + KB * D + i, rec + KB * D + KB + i, tag);
     }
 }
 
@@ -520,12 +844,13 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t)
 {
     using G = Geo<D, BF16>;
-    constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
+    using TL = Tile<D, BF16, KB>;
+    constexpr int kLpr = G::kLpr;
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
 
     __shared__ float m_lds[kWaves][KB], l_lds[kWaves][KB];
-    __shared__ float a_lds[kWaves][KB][D];
-    __shared__ __attribute__((aligned(16))) float p_lds[kWaves][G::kPStride][KB];
+    __shared__ __attribute__((aligned(16))) float a_lds[kWaves][KB][D];
+    __shared__ __attribute__((aligned(16))) char t_lds[kWaves][TL::kLdsBytes];
 
     // Workgroup g runs on XCD g % 8 (round-robin dispatch).  All chunks of
     // one (b, h), its generated-token workgroup and its merger get ids with
@@ -537,7 +862,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     if constexpr (SPLIT) {
         if (g < n_bh8) {
             attend_generated<D, BF16, KB>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
-                                          &p_lds[threadIdx.x / kWave][0][0]);
+                                          &t_lds[threadIdx.x / kWave][0]);
             return;
         }
         g -= n_bh8;
@@ -570,42 +895,17 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
 
     const int lane = tid & (kWave - 1);
     const int w = tid / kWave;
-    const int sub = lane % kLpr;  // 16-byte slice of the row this lane reads
-    const int grp = lane / kLpr;  // row of the instruction this lane reads
 
-    uint4 qr[KB];
-#pragma unroll
-    for (int i = 0; i < KB; ++i) qr[i] = q[((size_t)(b * KB + i) * H + h) * kLpr + sub];
-
+    typename TL::Q qv;
+    TL::load_q(qv, q, (size_t)b * KB, h, H, lane);
     const uint4 *Kbh = K + (size_t)bh * S * kLpr;
     const uint4 *Vbh = V + (size_t)bh * S * kLpr;
 
-    float m[KB], l[KB], acc[KB][kEpl];
-#pragma unroll
-    for (int i = 0; i < KB; ++i) {
-        m[i] = -INFINITY;
-        l[i] = 0.f;
-#pragma unroll
-        for (int e = 0; e < kEpl; ++e) acc[i][e] = 0.f;
-    }
-
+    typename TL::St st;
+    TL::init(st);
     const int t0 = j0 + w * kTile;
-    if (t0 < j1)
-        tile_attend<D, BF16, KB>(qr, Kbh, Vbh, t0, j1, sub, grp, &p_lds[w][0][0], scale_log2, m, l, acc);
-    if (lane < kLpr) {
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-#pragma unroll
-            for (int e = 0; e < kEpl; ++e) a_lds[w][i][sub * kEpl + e] = acc[i][e];
-        }
-    }
-    if (lane == 0) {
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-            m_lds[w][i] = m[i];
-            l_lds[w][i] = l[i];
-        }
-    }
+    if (t0 < j1) TL::attend(qv, Kbh, Vbh, t0, j1, lane, &t_lds[w][0], scale_log2, st);
+    TL::to_lds(st, lane, &m_lds[w][0], &l_lds[w][0], &a_lds[w][0][0]);
     __syncthreads();
 
     if (!SPLIT && nc == 1) {
@@ -650,15 +950,16 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     float scale_log2, const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t)
 {
     using G = Geo<D, BF16>;
-    constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
+    using TL = Tile<D, BF16, KB>;
+    constexpr int kLpr = G::kLpr;
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
     constexpr int kW = kWaves * P;                        // waves per workgroup
     constexpr int kThreads = kBlock * P;
     constexpr int kPer = (KB * D + kThreads - 1) / kThreads;  // outputs per thread
 
     __shared__ float m_lds[kW][KB], l_lds[kW][KB];
-    __shared__ float a_lds[kW][KB][D];
-    __shared__ __attribute__((aligned(16))) float p_lds[kW][G::kPStride][KB];
+    __shared__ __attribute__((aligned(16))) float a_lds[kW][KB][D];
+    __shared__ __attribute__((aligned(16))) char t_lds[kW][TL::kLdsBytes];
 
     const int bh = blockIdx.x;
     if (bh >= n_bh) return;
@@ -669,13 +970,10 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int w = tid / kWave;
-    const int sub = lane % kLpr;
-    const int grp = lane / kLpr;
     const size_t obase = ((size_t)b * KB * H + h) * D;  // out[b, 0, h, 0]
 
-    uint4 qr[KB];
-#pragma unroll
-    for (int i = 0; i < KB; ++i) qr[i] = q[((size_t)(b * KB + i) * H + h) * kLpr + sub];
+    typename TL::Q qv;
+    TL::load_q(qv, q, (size_t)b * KB, h, H, lane);
     const uint4 *Kbh = K + (size_t)bh * S * kLpr;
     const uint4 *Vbh = V + (size_t)bh * S * kLpr;
 
@@ -692,35 +990,15 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const int wt = w % kWaves;   // its tile in that chunk
     for (int c0 = 0; c0 < nc; c0 += P) {
         const int c = c0 + cg;
-        float m[KB], l[KB], acc[KB][kEpl];
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-            m[i] = -INFINITY;
-            l[i] = 0.f;
-#pragma unroll
-            for (int e = 0; e < kEpl; ++e) acc[i][e] = 0.f;
-        }
+        typename TL::St st;
+        TL::init(st);
         if (c < nc) {
             const int j0 = c * kChunk;
             const int j1 = min(j0 + kChunk, L);
             const int t0 = j0 + wt * kTile;
-            if (t0 < j1)
-                tile_attend<D, BF16, KB>(qr, Kbh, Vbh, t0, j1, sub, grp, &p_lds[w][0][0], scale_log2, m, l, acc);
+            if (t0 < j1) TL::attend(qv, Kbh, Vbh, t0, j1, lane, &t_lds[w][0], scale_log2, st);
         }
-        if (lane < kLpr) {
-#pragma unroll
-            for (int i = 0; i < KB; ++i) {
-#pragma unroll
-                for (int e = 0; e < kEpl; ++e) a_lds[w][i][sub * kEpl + e] = acc[i][e];
-            }
-        }
-        if (lane == 0) {
-#pragma unroll
-            for (int i = 0; i < KB; ++i) {
-                m_lds[w][i] = m[i];
-                l_lds[w][i] = l[i];
-            }
-        }
+        TL::to_lds(st, lane, &m_lds[w][0], &l_lds[w][0], &a_lds[w][0][0]);
         __syncthreads();
 #pragma unroll
         for (int p = 0; p < kPer; ++p) {
@@ -742,20 +1020,14 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     bool any = nc > 0;
     if constexpr (SPLIT) {
         if (t > 0) {
+            using T1 = Tile<D, BF16, 1>;
             any = true;
             // beam i's state over its own generated rows, kept in slot [0][i]
             for (int i = w; i < KB; i += kW) {
-                float m, l, acc[kEpl];
-                generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, sub, grp, &p_lds[w][0][0],
-                                         scale_log2, m, l, acc);
-                if (lane < kLpr) {
-#pragma unroll
-                    for (int e = 0; e < kEpl; ++e) a_lds[0][i][sub * kEpl + e] = acc[e];
-                }
-                if (lane == 0) {
-                    m_lds[0][i] = m;
-                    l_lds[0][i] = l;
-                }
+                typename T1::St st;
+                generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, &t_lds[w][0],
+                                         scale_log2, st);
+                T1::to_lds(st, lane, &m_lds[0][i], &l_lds[0][i], &a_lds[0][i][0]);
             }
             __syncthreads();
 #pragma unroll
@@ -777,6 +1049,7 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
         }
     }
 }
+
 
 // Launch arguments shared by both entry points.  For the encoder-decoder
 // form Kt/Vt are null and T = t = 0.
