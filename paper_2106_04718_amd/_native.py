@@ -1,8 +1,12 @@
-"""ctypes binding of libfastseq_hip.so (the C ABI declared in include/fastseq_hip.h).
+"""Bindings of libfastseq_hip.so (the C ABI declared in include/fastseq_hip.h).
 
-Only argument marshalling lives here.  The library must have been built
-(``__graft_entry__.build()`` or ``python -m paper_2106_04718_amd.build``);
-if it is missing every call raises -- there is no fallback path.
+Only argument marshalling lives here.  ``lib()`` is a ctypes handle on the
+library (every entry point, used for the size queries and the ABI tests);
+``ext()`` is the CPython module built from csrc/pyext.c, which the launch
+calls go through because it converts arguments in a fraction of ctypes'
+time.  Both must have been built (``__graft_entry__.build()`` or
+``python -m paper_2106_04718_amd.build``); if either is missing every call
+raises -- there is no fallback path.
 """
 import ctypes
 import pathlib
@@ -33,6 +37,7 @@ SIGNATURES = [
 ]
 
 _lib = None
+_ext = None
 
 
 class NativeError(RuntimeError):
@@ -60,6 +65,20 @@ def lib() -> ctypes.CDLL:
     return _lib
 
 
+def ext():
+    """The CPython marshalling module; raise if it was never built."""
+    global _ext
+    if _ext is None:
+        lib()
+        try:
+            from . import _fastseq_ext
+        except ImportError as e:
+            raise RuntimeError("the _fastseq_ext module is not built; run __graft_entry__.build() "
+                               "(no CPU fallback exists for the decode-step kernels)") from e
+        _ext = _fastseq_ext
+    return _ext
+
+
 def status_string(status: int) -> str:
     return lib().fs_status_string(status).decode()
 
@@ -69,5 +88,6 @@ def last_error() -> str:
 
 
 def check(status: int) -> None:
+    """Raise on a non-OK status of a call made through ext()."""
     if status != FS_OK:
-        raise NativeError(status, last_error())
+        raise NativeError(status, ext().fs_last_error())

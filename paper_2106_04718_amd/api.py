@@ -3,8 +3,16 @@
 Each function checks tensor placement, dtype and layout, then passes raw
 device pointers and torch's current HIP stream to the C ABI.  PyTorch only
 provides memory and streams here; all arithmetic runs in the HIP kernels.
+
+A decode step is a few tens of microseconds of GPU time, so the per-call
+host work is kept small: workspace sizes are cached per shape, the stream
+handle is read without building a Stream object, the device is switched
+only when the tensors are not on the current one, and the call itself goes
+through the CPython marshalling module rather than ctypes.
 """
 from __future__ import annotations
+
+import contextlib
 
 import torch
 
@@ -12,10 +20,23 @@ from . import _native as _N
 
 _native_lib = _N.lib
 _DTYPES = {torch.float32: _N.FS_F32, torch.bfloat16: _N.FS_BF16}
+_WS_BYTES: dict = {}
+
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None) or torch.cuda.current_device
 
 
 def _stream_ptr(device: torch.device) -> int:
+    if _raw_stream is not None:
+        return _raw_stream(device.index)
     return torch.cuda.current_stream(device).cuda_stream
+
+
+def _on(device: torch.device):
+    """A device guard, or nothing if ``device`` is already current."""
+    if device.index == _cur_device():
+        return contextlib.nullcontext()
+    return torch.cuda.device(device)
 
 
 def _need_cuda(name: str, t: torch.Tensor) -> None:
@@ -35,13 +56,21 @@ def new_workspace(nbytes: int, device) -> torch.Tensor:
     return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
-def beam_cross_attn_workspace_bytes(B: int, k: int, H: int, S: int, D: int,
-                                    dtype: torch.dtype = torch.bfloat16) -> int:
-    """Bytes of fp32 workspace fs_beam_cross_attn needs for these sizes."""
-    n = _N.lib().fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, _DTYPES[dtype])
+def _size_or_raise(n: int) -> int:
     if n == 2**64 - 1:
         raise _N.NativeError(_N.FS_ERR_UNSUPPORTED, _N.last_error())
     return int(n)
+
+
+def beam_cross_attn_workspace_bytes(B: int, k: int, H: int, S: int, D: int,
+                                    dtype: torch.dtype = torch.bfloat16) -> int:
+    """Bytes of workspace fs_beam_cross_attn needs for these sizes."""
+    key = ("x", B, k, H, S, D, dtype)
+    n = _WS_BYTES.get(key)
+    if n is None:
+        n = _size_or_raise(_N.lib().fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, _DTYPES[dtype]))
+        _WS_BYTES[key] = n
+    return n
 
 
 def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: torch.Tensor,
@@ -62,12 +91,13 @@ def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: 
     if K.shape[0] != B or K.shape[1] != H or K.shape[3] != D:
         raise ValueError(f"shape mismatch: q{tuple(q.shape)} K{tuple(K.shape)}")
     S = K.shape[2]
-    if q.dtype not in _DTYPES or K.dtype != q.dtype or V.dtype != q.dtype:
+    dt = _DTYPES.get(q.dtype)
+    if dt is None or K.dtype != q.dtype or V.dtype != q.dtype:
         raise ValueError("q, K and V must all be float32 or all bfloat16")
     if src_len.dtype != torch.int32 or src_len.shape != (B,):
         raise ValueError("src_len must be int32 [B]")
     dev = q.device
-    if any(t.device != dev for t in (K, V, src_len)):
+    if K.device != dev or V.device != dev or src_len.device != dev:
         raise ValueError("all tensors must be on one device")
     if out is None:
         out = torch.empty_like(q)
@@ -75,14 +105,12 @@ def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: 
         _need_cuda("out", out)
         if out.shape != q.shape or out.dtype != q.dtype or out.device != dev:
             raise ValueError("out must match q in shape, dtype and device")
-    dt = _DTYPES[q.dtype]
-    need = beam_cross_attn_workspace_bytes(B, k, H, S, D, q.dtype)
     if workspace is None:
-        workspace = new_workspace(need, dev)
+        workspace = new_workspace(beam_cross_attn_workspace_bytes(B, k, H, S, D, q.dtype), dev)
     else:
         _need_cuda("workspace", workspace)
-    with torch.cuda.device(dev):
-        _N.check(_N.lib().fs_beam_cross_attn(
+    with _on(dev):
+        _N.check(_N.ext().fs_beam_cross_attn(
             q.data_ptr(), K.data_ptr(), V.data_ptr(), src_len.data_ptr(), out.data_ptr(),
             B, k, H, S, D, dt, workspace.data_ptr(), workspace.numel() * workspace.element_size(),
             _stream_ptr(dev)))
@@ -92,10 +120,12 @@ def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: 
 def beam_prefix_attn_workspace_bytes(B: int, k: int, H: int, N: int, T: int, D: int,
                                      dtype: torch.dtype = torch.bfloat16) -> int:
     """Bytes of workspace fs_beam_prefix_attn needs for these sizes."""
-    n = _native_lib().fs_beam_prefix_attn_workspace_bytes(B, k, H, N, T, D, _DTYPES[dtype])
-    if n == 2**64 - 1:
-        raise _N.NativeError(_N.FS_ERR_UNSUPPORTED, _N.last_error())
-    return int(n)
+    key = ("p", B, k, H, N, T, D, dtype)
+    n = _WS_BYTES.get(key)
+    if n is None:
+        n = _size_or_raise(_native_lib().fs_beam_prefix_attn_workspace_bytes(B, k, H, N, T, D, _DTYPES[dtype]))
+        _WS_BYTES[key] = n
+    return n
 
 
 def beam_prefix_attn(q: torch.Tensor, Kp: torch.Tensor, Vp: torch.Tensor, prefix_len: torch.Tensor,
@@ -128,13 +158,12 @@ def beam_prefix_attn(q: torch.Tensor, Kp: torch.Tensor, Vp: torch.Tensor, prefix
         _need_cuda("out", out)
         if out.shape != q.shape or out.dtype != q.dtype or out.device != dev:
             raise ValueError("out must match q in shape, dtype and device")
-    need = beam_prefix_attn_workspace_bytes(B, k, H, Np, T, D, q.dtype)
     if workspace is None:
-        workspace = new_workspace(need, dev)
+        workspace = new_workspace(beam_prefix_attn_workspace_bytes(B, k, H, Np, T, D, q.dtype), dev)
     else:
         _need_cuda("workspace", workspace)
-    with torch.cuda.device(dev):
-        _N.check(_native_lib().fs_beam_prefix_attn(
+    with _on(dev):
+        _N.check(_N.ext().fs_beam_prefix_attn(
             q.data_ptr(), Kp.data_ptr(), Vp.data_ptr(), prefix_len.data_ptr(), Kt.data_ptr(), Vt.data_ptr(),
             T, int(t), out.data_ptr(), B, k, H, Np, D, _DTYPES[q.dtype], workspace.data_ptr(),
             workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
@@ -153,20 +182,20 @@ def ngram_block(tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | Non
     _need_cuda("logits", logits)
     if tokens.dim() != 2 or tokens.dtype != torch.int32:
         raise ValueError("tokens must be int32 [rows, ld]")
-    if tokens.numel() > 0 and tokens.shape[1] > 1 and tokens.stride(1) != 1:
+    rows, cols = tokens.shape
+    if rows > 0 and cols > 1 and tokens.stride(1) != 1:
         raise ValueError("tokens must have unit column stride")
     if logits.dim() != 2 or logits.dtype != torch.float32:
         raise ValueError("logits must be float32 [rows, V]")
-    rows = tokens.shape[0]
-    if logits.shape[0] != rows or logits.device != tokens.device:
-        raise ValueError("tokens and logits must have the same rows and device")
-    ld = tokens.stride(0) if rows > 1 else tokens.shape[1]
-    if t is None:
-        t = tokens.shape[1]
-    if t > tokens.shape[1]:
-        raise ValueError("t exceeds the columns of tokens")
     dev = tokens.device
-    with torch.cuda.device(dev):
-        _N.check(_N.lib().fs_ngram_block(tokens.data_ptr(), ld, rows, int(t), int(n),
-                                       logits.data_ptr(), logits.shape[1], _stream_ptr(dev)))
+    if logits.shape[0] != rows or logits.device != dev:
+        raise ValueError("tokens and logits must have the same rows and device")
+    ld = tokens.stride(0) if rows > 1 else cols
+    if t is None:
+        t = cols
+    if t > cols:
+        raise ValueError("t exceeds the columns of tokens")
+    with _on(dev):
+        _N.check(_N.ext().fs_ngram_block(tokens.data_ptr(), ld, rows, int(t), int(n),
+                                         logits.data_ptr(), logits.shape[1], _stream_ptr(dev)))
     return logits

@@ -3,18 +3,23 @@
 Every source is compiled with hipcc for gfx950 only.  Packed-fp32 VALU
 instructions are disabled for device code (``-packed-fp32-ops``); the host
 pass warns that it does not know that feature, which is harmless.
+
+The CPython marshalling module (csrc/pyext.c, plain C) is then compiled with
+gcc and linked against the library.
 """
 import concurrent.futures
 import os
 import pathlib
 import subprocess
+import sysconfig
 
 PKG = pathlib.Path(__file__).resolve().parent
 ROOT = PKG.parent
 CSRC = PKG / "csrc"
 BUILD = PKG / "_build"
 LIB = PKG / "libfastseq_hip.so"
-SOURCES = ["capi.cpp", "cross_attn.hip", "ngram_block.hip"]
+EXT = PKG / ("_fastseq_ext" + sysconfig.get_config_var("EXT_SUFFIX"))
+SOURCES = ["capi.cpp", "cross_attn.hip", "ngram_block.hip"]  # pyext.c is built by build_ext
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -48,12 +53,27 @@ def build(verbose: bool = False) -> pathlib.Path:
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
     tmp = str(LIB) + ".tmp"
-    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *map(str, objs), "-o", tmp]
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-Wl,-soname,libfastseq_hip.so",
+           *map(str, objs), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    build_ext(verbose)
     return LIB
+
+
+def build_ext(verbose: bool = False) -> pathlib.Path:
+    """The CPython module that marshals arguments into the C ABI."""
+    tmp = str(EXT) + ".tmp"
+    cmd = ["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror",
+           f"-I{sysconfig.get_paths()['include']}", f"-I{ROOT / 'include'}", str(CSRC / "pyext.c"),
+           f"-L{PKG}", "-lfastseq_hip", "-Wl,-rpath,$ORIGIN", "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, EXT)
+    return EXT
 
 
 if __name__ == "__main__":

@@ -138,3 +138,25 @@ def test_validation_runs_before_any_hip_call():
     # status is the argument error, not FS_ERR_HIP.
     assert attn(D=48) == N.FS_ERR_UNSUPPORTED
     assert ngram(n=0) == N.FS_ERR_INVALID_ARG
+
+
+def test_marshalling_module_reaches_the_same_library():
+    # The launch calls go through the CPython module built from pyext.c; it
+    # must bind the very library that ctypes loads (one copy, one
+    # thread-local error slot), and pass every argument through unchanged.
+    E = N.ext()
+    for name in ("fs_beam_cross_attn", "fs_beam_prefix_attn", "fs_ngram_block", "fs_last_error"):
+        assert callable(getattr(E, name)), name
+    assert E.fs_ngram_block(FAKE, 4, 2, 5, 3, FAKE * 2, 7, None) == N.FS_ERR_INVALID_ARG
+    assert "ld_tokens=4 < t=5" in E.fs_last_error()
+    assert "ld_tokens=4 < t=5" in N.last_error()
+    st = E.fs_beam_cross_attn(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, FAKE * 5, 2, 9, 2, 64, 16, N.FS_F32,
+                              FAKE * 6, 1 << 30, None)
+    assert st == N.FS_ERR_UNSUPPORTED and "k=9" in E.fs_last_error()
+    st = E.fs_beam_prefix_attn(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 3, 4, FAKE, 1, 1, 1, 1, 16, N.FS_F32,
+                               FAKE, 1 << 20, None)
+    assert st == N.FS_ERR_INVALID_ARG and "t=4 exceeds" in E.fs_last_error()
+    with pytest.raises(TypeError):
+        E.fs_ngram_block(FAKE, 4, 2)
+    with pytest.raises(OverflowError):
+        E.fs_ngram_block(FAKE, 1 << 40, 2, 5, 3, FAKE * 2, 7, None)
