@@ -80,6 +80,17 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
     return make_uint4(t.x, t.y, t.z, t.w);
 }
 
+// Buffer resource over the first `bytes` bytes at p (raw addressing, no
+// stride): loads past the end return zero without touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void *p, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, bytes, 0x00020000);
+}
+// 16-byte non-temporal buffer load at byte offset voff + soff.
+__device__ __forceinline__ uint4 load_rows(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    const u32x4_t t = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 2));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -237,6 +248,12 @@ __device__ __forceinline__ void group_reduce_scatter(float (&d)[NI][KB], int sub
             group_reduce_scatter<G, KB, NI, MASK / 2, 1>(d, sub);
         }
     }
+}
+
+// Index of this wave in its workgroup, as a wave-uniform (scalar) value, so
+// that branches on it are uniform and each side keeps its own registers.
+__device__ __forceinline__ int wave_id() {
+    return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
 }
 
 // Merge softmax state (mb, lb, ab) into (m, l, a); m in the base-2 domain.
@@ -554,15 +571,19 @@ struct MfmaTile {
         const int n = lane & 15, g = lane >> 4;
         // Row loads in the coalesced layout: kLpr lanes per row, so one
         // instruction reads whole rows (loads of 16 half rows each are
-        // markedly slower).  Rows past j1 re-read row j1 - 1 and are masked.
-        // All K first, so its trip through LDS can start while V is in flight.
+        // markedly slower).  Buffer loads whose range ends at row j1: rows
+        // past it read as zero without a memory access and are masked, and
+        // K and V share one offset register.  All K first, so its trip
+        // through LDS can start while V is in flight.
         constexpr int kRpi = kWave / kLpr;
         const int sub = lane % kLpr, grp = lane / kLpr;
+        const auto kres = row_rsrc(Kb, j1 * 2 * D), vres = row_rsrc(Vb, j1 * 2 * D);
+        const int off = ((t0 + grp) * kLpr + sub) * 16;
         uint4 kr[kIt], vr[kIt];
 #pragma unroll
-        for (int u = 0; u < kIt; ++u) kr[u] = load_nt(Kb + (size_t)min(t0 + u * kRpi + grp, j1 - 1) * kLpr + sub);
+        for (int u = 0; u < kIt; ++u) kr[u] = load_rows(kres, off, u * kRpi * 2 * D);
 #pragma unroll
-        for (int u = 0; u < kIt; ++u) vr[u] = load_nt(Vb + (size_t)min(t0 + u * kRpi + grp, j1 - 1) * kLpr + sub);
+        for (int u = 0; u < kIt; ++u) vr[u] = load_rows(vres, off, u * kRpi * 2 * D);
         // K through LDS into the MFMA A layout: lane l takes row 16 kb + n,
         // dims 32 s + 8 g .. + 8
         char *vt = static_cast<char *>(lds);
@@ -677,6 +698,14 @@ struct MfmaTile {
 
 template <int D, bool BF16, int KB>
 using Tile = typename std::conditional<(BF16 && D >= 32), MfmaTile<D, KB>, ValuTile<D, BF16, KB>>::type;
+
+// LDS area of one wave: large enough for a tile of KB beams or of one beam,
+// and for the wave's acc[KB][D] once its tile is done (16-byte multiple).
+template <int D, bool BF16, int KB>
+struct WaveLds {
+    static constexpr int a = Tile<D, BF16, KB>::kLdsBytes, b = Tile<D, BF16, 1>::kLdsBytes, c = KB * D * 4;
+    static constexpr int kBytes = ((a > b ? (a > c ? a : c) : (b > c ? b : c)) + 15) / 16 * 16;
+};
 
 
 template <int D, bool BF16, int KB>
@@ -824,7 +853,7 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     const int b = bh / H;
     const int h = bh - b * H;
     const int lane = threadIdx.x & (kWave - 1);
-    const int w = threadIdx.x / kWave;
+    const int w = wave_id();
     constexpr int kRec = KB * (D + 2);
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
@@ -849,8 +878,9 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
 
     __shared__ float m_lds[kWaves][KB], l_lds[kWaves][KB];
-    __shared__ __attribute__((aligned(16))) float a_lds[kWaves][KB][D];
-    __shared__ __attribute__((aligned(16))) char t_lds[kWaves][TL::kLdsBytes];
+    // each wave's tile area, which then holds its acc[KB][D] for the merge
+    __shared__ __attribute__((aligned(16))) char t_lds[kWaves][WaveLds<D, BF16, KB>::kBytes];
+    auto a_lds = [&](int ww) { return reinterpret_cast<float *>(&t_lds[ww][0]); };
 
     // Workgroup g runs on XCD g % 8 (round-robin dispatch).  All chunks of
     // one (b, h), its generated-token workgroup and its merger get ids with
@@ -862,7 +892,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     if constexpr (SPLIT) {
         if (g < n_bh8) {
             attend_generated<D, BF16, KB>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
-                                          &t_lds[threadIdx.x / kWave][0]);
+                                          &t_lds[wave_id()][0]);
             return;
         }
         g -= n_bh8;
@@ -894,7 +924,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const int j1 = min(j0 + kChunk, L);
 
     const int lane = tid & (kWave - 1);
-    const int w = tid / kWave;
+    const int w = wave_id();
 
     typename TL::Q qv;
     TL::load_q(qv, q, (size_t)b * KB, h, H, lane);
@@ -905,15 +935,15 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     TL::init(st);
     const int t0 = j0 + w * kTile;
     if (t0 < j1) TL::attend(qv, Kbh, Vbh, t0, j1, lane, &t_lds[w][0], scale_log2, st);
-    TL::to_lds(st, lane, &m_lds[w][0], &l_lds[w][0], &a_lds[w][0][0]);
+    TL::to_lds(st, lane, &m_lds[w][0], &l_lds[w][0], a_lds(w));
     __syncthreads();
 
     if (!SPLIT && nc == 1) {
         for (int x = tid; x < KB * D; x += kBlock) {
             const int i = x / D, d = x - i * D;
-            float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds[0][i][d];
+            float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * D + d];
 #pragma unroll
-            for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds[ww][i][d]);
+            for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * D + d]);
             store_out<BF16>(out, obase + (size_t)i * H * D + d, aa / ll);
         }
         return;
@@ -924,9 +954,9 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     for (int x = tid; x < KB * D; x += kBlock) {
         const int i = x / D, d = x - i * D;
-        float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds[0][i][d];
+        float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * D + d];
 #pragma unroll
-        for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds[ww][i][d]);
+        for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * D + d]);
         store_word(rec + x, tag, aa);
         if (d == 0) {
             store_word(rec + KB * D + i, tag, mm);
@@ -936,13 +966,15 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
 }
 
 // One workgroup per (b, h) that walks all of its chunks itself: no partial
-// records, no merger, no cross-workgroup wait.  P chunks are processed at a
+// records, no merger, no cross-workgroup wait.  The row's jobs -- its chunks
+// and, for the split cache, the generated tokens -- are processed P at a
 // time by P groups of kWaves waves (workgroup of P*kBlock threads).  The
-// arithmetic and its order are those of cross_attn_kernel -- each chunk's
-// four wave states merged in wave order, the chunk states folded in chunk
-// order from the empty state, the generated-token state (SPLIT) last -- so
-// both kernels give the same bits.  It pays when there are enough (b, h)
-// rows to fill the chip without splitting them.
+// generated-token job goes first, so that its tiles are read alongside the
+// first chunks, but it is folded last.  The arithmetic and its order are
+// those of cross_attn_kernel -- each chunk's four wave states merged in wave
+// order, the chunk states folded in chunk order from the empty state, the
+// generated-token state last -- so both kernels give the same bits.  It pays
+// when there are enough (b, h) rows to fill the chip without splitting them.
 template <int D, bool BF16, int KB, bool SPLIT, int P>
 __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
@@ -951,15 +983,20 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
 {
     using G = Geo<D, BF16>;
     using TL = Tile<D, BF16, KB>;
+    using T1 = Tile<D, BF16, 1>;
     constexpr int kLpr = G::kLpr;
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
     constexpr int kW = kWaves * P;                        // waves per workgroup
     constexpr int kThreads = kBlock * P;
     constexpr int kPer = (KB * D + kThreads - 1) / kThreads;  // outputs per thread
+    constexpr int kGB = SPLIT ? KB : 1, kGD = SPLIT ? D : 1;
 
     __shared__ float m_lds[kW][KB], l_lds[kW][KB];
-    __shared__ __attribute__((aligned(16))) float a_lds[kW][KB][D];
-    __shared__ __attribute__((aligned(16))) char t_lds[kW][TL::kLdsBytes];
+    // each wave's tile area, which then holds its acc[KB][D] for the merge
+    __shared__ __attribute__((aligned(16))) char t_lds[kW][WaveLds<D, BF16, KB>::kBytes];
+    // generated-token states, kept until they are folded in at the end
+    __shared__ __attribute__((aligned(16))) float g_lds[kGB][kGD];
+    __shared__ float gm_lds[kGB], gl_lds[kGB];
 
     const int bh = blockIdx.x;
     if (bh >= n_bh) return;
@@ -969,7 +1006,7 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const int nc = (L + kChunk - 1) / kChunk;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int w = tid / kWave;
+    const int w = wave_id();
     const size_t obase = ((size_t)b * KB * H + h) * D;  // out[b, 0, h, 0]
 
     typename TL::Q qv;
@@ -986,60 +1023,64 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
         Ra[p] = 0.f;
     }
 
-    const int cg = w / kWaves;   // chunk of the step this wave works on
-    const int wt = w % kWaves;   // its tile in that chunk
-    for (int c0 = 0; c0 < nc; c0 += P) {
-        const int c = c0 + cg;
-        typename TL::St st;
-        TL::init(st);
-        if (c < nc) {
-            const int j0 = c * kChunk;
-            const int j1 = min(j0 + kChunk, L);
-            const int t0 = j0 + wt * kTile;
+    // jobs: [generated tokens (SPLIT, t > 0)] chunk 0, chunk 1, ...
+    const int ng = (SPLIT && t > 0) ? 1 : 0;
+    const int njobs = nc + ng;
+    const int cg = w / kWaves;   // group of this wave: job j0 + cg of each step
+    const int wt = w % kWaves;   // its wave in the group
+    for (int j0 = 0; j0 < njobs; j0 += P) {
+        const int c = j0 + cg - ng;  // chunk of this group's job; -1: generated tokens
+        if (j0 + cg < njobs && c < 0) {
+            if constexpr (SPLIT) {
+                // beam i's state over its own generated rows
+                for (int i = wt; i < KB; i += kWaves) {
+                    typename T1::St gst;
+                    generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, &t_lds[w][0],
+                                             scale_log2, gst);
+                    T1::to_lds(gst, lane, &gm_lds[i], &gl_lds[i], &g_lds[i][0]);
+                }
+            }
+        } else if (j0 + cg < njobs) {
+            typename TL::St st;
+            TL::init(st);
+            const int j1 = min((c + 1) * kChunk, L);
+            const int t0 = c * kChunk + wt * kTile;
             if (t0 < j1) TL::attend(qv, Kbh, Vbh, t0, j1, lane, &t_lds[w][0], scale_log2, st);
+            TL::to_lds(st, lane, &m_lds[w][0], &l_lds[w][0], reinterpret_cast<float *>(&t_lds[w][0]));
         }
-        TL::to_lds(st, lane, &m_lds[w][0], &l_lds[w][0], &a_lds[w][0][0]);
         __syncthreads();
 #pragma unroll
         for (int p = 0; p < kPer; ++p) {
             const int x = tid + p * kThreads;
             if (x < KB * D) {
                 const int i = x / D, d = x - i * D;
-                for (int g = 0; g < P && c0 + g < nc; ++g) {
+                for (int g = 0; g < P && j0 + g < njobs; ++g) {
+                    if (j0 + g < ng) continue;  // the generated-token job is folded last
                     const int w0 = g * kWaves;
-                    float mm = m_lds[w0][i], ll = l_lds[w0][i], aa = a_lds[w0][i][d];
+                    const float *a0 = reinterpret_cast<const float *>(&t_lds[w0][0]);
+                    float mm = m_lds[w0][i], ll = l_lds[w0][i], aa = a0[i * D + d];
 #pragma unroll
-                    for (int ww = 1; ww < kWaves; ++ww)
-                        merge_state(mm, ll, aa, m_lds[w0 + ww][i], l_lds[w0 + ww][i], a_lds[w0 + ww][i][d]);
+                    for (int ww = 1; ww < kWaves; ++ww) {
+                        const float *aw = reinterpret_cast<const float *>(&t_lds[w0 + ww][0]);
+                        merge_state(mm, ll, aa, m_lds[w0 + ww][i], l_lds[w0 + ww][i], aw[i * D + d]);
+                    }
                     merge_state(Rm[p], Rl[p], Ra[p], mm, ll, aa);
                 }
             }
         }
         __syncthreads();
     }
-    bool any = nc > 0;
-    if constexpr (SPLIT) {
-        if (t > 0) {
-            using T1 = Tile<D, BF16, 1>;
-            any = true;
-            // beam i's state over its own generated rows, kept in slot [0][i]
-            for (int i = w; i < KB; i += kW) {
-                typename T1::St st;
-                generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, &t_lds[w][0],
-                                         scale_log2, st);
-                T1::to_lds(st, lane, &m_lds[0][i], &l_lds[0][i], &a_lds[0][i][0]);
-            }
-            __syncthreads();
+    if (ng) {
 #pragma unroll
-            for (int p = 0; p < kPer; ++p) {
-                const int x = tid + p * kThreads;
-                if (x < KB * D) {
-                    const int i = x / D, d = x - i * D;
-                    merge_state(Rm[p], Rl[p], Ra[p], m_lds[0][i], l_lds[0][i], a_lds[0][i][d]);
-                }
+        for (int p = 0; p < kPer; ++p) {
+            const int x = tid + p * kThreads;
+            if (x < KB * D) {
+                const int i = x / D, d = x - i * D;
+                merge_state(Rm[p], Rl[p], Ra[p], gm_lds[i], gl_lds[i], g_lds[i][d]);
             }
         }
     }
+    const bool any = njobs > 0;
 #pragma unroll
     for (int p = 0; p < kPer; ++p) {
         const int x = tid + p * kThreads;
@@ -1049,7 +1090,6 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
         }
     }
 }
-
 
 // Launch arguments shared by both entry points.  For the encoder-decoder
 // form Kt/Vt are null and T = t = 0.
@@ -1102,9 +1142,11 @@ hipError_t launch_typed(const AttnArgs &a)
     // at least one chunk column, so that a source with no valid key (or
     // S == 0) still has a workgroup to write its zero output
     const int NC = max(1, (a.S + G::kChunk - 1) / G::kChunk);
-    switch (choose_attn_path(a.B * a.H, NC)) {
+    // jobs per row: its chunks, plus the generated tokens of the split cache
+    switch (choose_attn_path(a.B * a.H, NC + (SPLIT && a.t > 0 ? 1 : 0))) {
     case AttnPath::kWhole1: return launch_whole<D, BF16, KB, SPLIT, 1>(a);
     case AttnPath::kWhole2: return launch_whole<D, BF16, KB, SPLIT, 2>(a);
+    case AttnPath::kWhole4: return launch_whole<D, BF16, KB, SPLIT, 4>(a);
     default: return launch_split<D, BF16, KB, SPLIT>(a, NC);
     }
 }
@@ -1139,11 +1181,12 @@ hipError_t launch_d(const AttnArgs &a)
 
 }  // namespace
 
-AttnPath choose_attn_path(int n_bh, int nc_max) {
+AttnPath choose_attn_path(int n_bh, int jobs_max) {
     if (const char *v = getenv("FS_ATTN_PATH")) {
         if (!strcmp(v, "split")) return AttnPath::kSplit;
         if (!strcmp(v, "whole1")) return AttnPath::kWhole1;
         if (!strcmp(v, "whole2")) return AttnPath::kWhole2;
+        if (!strcmp(v, "whole4")) return AttnPath::kWhole4;
     }
     // Measured on MI355X (bf16, D = 64, k = 4; 192 to 5120 rows of up to
     // 1024 keys): with four or more rows per CU, one 4-wave workgroup per
@@ -1151,8 +1194,8 @@ AttnPath choose_attn_path(int n_bh, int nc_max) {
     // per row (two chunks in flight) beats splitting rows across
     // workgroups, whose merge costs a round trip through memory.  Only a
     // few long rows are split.
-    if (nc_max <= 1 || n_bh >= kWhole1MinRows) return AttnPath::kWhole1;
-    if (n_bh >= kWhole2MinRows || nc_max <= 2) return AttnPath::kWhole2;
+    if (jobs_max <= 1 || n_bh >= kWhole1MinRows) return AttnPath::kWhole1;
+    if (n_bh >= kWhole2MinRows || jobs_max <= 2) return AttnPath::kWhole2;
     return AttnPath::kSplit;
 }
 

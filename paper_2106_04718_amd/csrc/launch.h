@@ -20,11 +20,12 @@ int cross_attn_chunk_keys(int D, int esize);
 //            trailing merger workgroups -- most parallel, pays a merge;
 //   kWholeP  one workgroup per (b, h) of P*4 waves walking its chunks P at a
 //            time -- no records, needs many (b, h) rows to fill the chip.
-enum class AttnPath { kAuto = 0, kSplit, kWhole1, kWhole2 };
+enum class AttnPath { kAuto = 0, kSplit, kWhole1, kWhole2, kWhole4 };
 
-// The path for n_bh = B*H rows of at most nc_max chunks: FS_ATTN_PATH
-// (split, whole1, whole2; read at every call) overrides the size rule.
-AttnPath choose_attn_path(int n_bh, int nc_max);
+// The path for n_bh = B*H rows of at most jobs_max jobs (chunks, plus the
+// generated tokens of the split cache): FS_ATTN_PATH
+// (split, whole1, whole2, whole4; read at every call) overrides the size rule.
+AttnPath choose_attn_path(int n_bh, int jobs_max);
 
 // Workspace size in 4-byte words: the per-chunk partial records (plus one
 // record per (b, h) for the generated-token segment when `split`).

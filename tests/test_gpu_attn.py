@@ -171,7 +171,7 @@ def test_workspace_reused_across_calls_with_changing_lengths():
     assert_attn_close(run(d, ws=ws), oracle_attn(d), "smaller problem, same workspace")
 
 
-PATHS = ("split", "whole1", "whole2")
+PATHS = ("split", "whole1", "whole2", "whole4")
 
 
 def run_path(path, fn):

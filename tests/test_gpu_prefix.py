@@ -149,7 +149,7 @@ def test_decompositions_give_identical_bits(dtype, D, k, t):
     outs = {}
     old = os.environ.get("FS_ATTN_PATH")
     try:
-        for p in ("split", "whole1", "whole2"):
+        for p in ("split", "whole1", "whole2", "whole4"):
             os.environ["FS_ATTN_PATH"] = p
             outs[p] = bits(run(d))
     finally:
@@ -159,4 +159,5 @@ def test_decompositions_give_identical_bits(dtype, D, k, t):
             os.environ["FS_ATTN_PATH"] = old
     assert np.array_equal(outs["whole1"], outs["split"])
     assert np.array_equal(outs["whole2"], outs["split"])
+    assert np.array_equal(outs["whole4"], outs["split"])
     assert_attn_close(run(d), ref(d), f"paths {dtype} D={D} k={k} t={t}")
