@@ -49,8 +49,8 @@ constexpr int kWaves = 4;
 constexpr int kBlock = kWave * kWaves;
 constexpr int kIt = 8;   // row loads of K (and of V) per lane per tile
 constexpr int kXcds = 8; // MI355X: workgroups go round-robin to 8 XCDs
-constexpr int kWhole1MinRows = 4 * 256;  // (b, h) rows for one 4-wave workgroup per row (256 CUs)
-constexpr int kWhole2MinRows = 128;      // rows for one 8-wave workgroup per row
+constexpr int kCus = 256;                // MI355X compute units
+constexpr int kWhole2MinRows = 128;      // fewer (b, h) rows than this are split across workgroups
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -433,19 +433,6 @@ struct ValuTile {
         tile_attend<D, BF16, KB>(q.r, Kb, Vb, t0, j1, lane % kLpr, lane / kLpr, static_cast<float *>(lds),
                                  scale_log2, s.m, s.l, s.acc);
     }
-    // fold the state of a later tile into the running state
-    static __device__ __forceinline__ void fold(St &s, const St &t) {
-#pragma unroll
-        for (int i = 0; i < KB; ++i) {
-            const float mx = fmaxf(s.m[i], t.m[i]);
-            const float fo = __builtin_amdgcn_exp2f(s.m[i] - mx);
-            const float fn = __builtin_amdgcn_exp2f(t.m[i] - mx);
-            s.l[i] = s.l[i] * fo + t.l[i] * fn;
-#pragma unroll
-            for (int e = 0; e < kEpl; ++e) s.acc[i][e] = s.acc[i][e] * fo + t.acc[i][e] * fn;
-            s.m[i] = mx;
-        }
-    }
     // this wave's state into LDS: m_w[KB], l_w[KB], a_w[KB][D]
     static __device__ __forceinline__ void to_lds(const St &s, int lane, float *m_w, float *l_w, float *a_w) {
         if (lane < kLpr) {
@@ -463,10 +450,6 @@ struct ValuTile {
             }
         }
     }
-    // beam 0's state as tagged record words: acc[D] at acc_w, then m, l
-    static __device__ __forceinline__ void to_record(const St &s, int lane, unsigned long long *acc_w,
-                                                     unsigned long long *m_w, unsigned long long *l_w,
-                                                     unsigned long long tag);
 };
 
 // Value of x in lanes l & ~MASK and l | MASK (MASK = 16 or 32), in that
@@ -668,18 +651,6 @@ struct MfmaTile {
 #pragma unroll
         for (int mb = 0; mb < NU; ++mb) st.acc[mb] = o[mb];
     }
-    static __device__ __forceinline__ void fold(St &s, const St &t) {
-        const float mx = fmaxf(s.m, t.m);
-        const float fo = __builtin_amdgcn_exp2f(s.m - mx);
-        const float fn = __builtin_amdgcn_exp2f(t.m - mx);
-        s.l = s.l * fo + t.l * fn;
-#pragma unroll
-        for (int mb = 0; mb < NU; ++mb) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) s.acc[mb][i] = s.acc[mb][i] * fo + t.acc[mb][i] * fn;
-        }
-        s.m = mx;
-    }
     static __device__ __forceinline__ void to_lds(const St &s, int lane, float *m_w, float *l_w, float *a_w) {
         const int n = lane & 15, g = lane >> 4;
         if (n < KB) {
@@ -691,54 +662,20 @@ struct MfmaTile {
             }
         }
     }
-    static __device__ __forceinline__ void to_record(const St &s, int lane, unsigned long long *acc_w,
-                                                     unsigned long long *m_w, unsigned long long *l_w,
-                                                     unsigned long long tag);
 };
 
 template <int D, bool BF16, int KB>
 using Tile = typename std::conditional<(BF16 && D >= 32), MfmaTile<D, KB>, ValuTile<D, BF16, KB>>::type;
 
 // LDS area of one wave: large enough for a tile of KB beams or of one beam,
-// and for the wave's acc[KB][D] once its tile is done (16-byte multiple).
+// for the wave's acc[KB][D] once its tile is done, and for one generated-
+// token tile state (m, l, acc[D] at float 4); a 16-byte multiple.
 template <int D, bool BF16, int KB>
 struct WaveLds {
-    static constexpr int a = Tile<D, BF16, KB>::kLdsBytes, b = Tile<D, BF16, 1>::kLdsBytes, c = KB * D * 4;
+    static constexpr int a = Tile<D, BF16, KB>::kLdsBytes, b = Tile<D, BF16, 1>::kLdsBytes;
+    static constexpr int c = KB * D * 4 > (D + 4) * 4 ? KB * D * 4 : (D + 4) * 4;
     static constexpr int kBytes = ((a > b ? (a > c ? a : c) : (b > c ? b : c)) + 15) / 16 * 16;
 };
-
-
-template <int D, bool BF16, int KB>
-__device__ __forceinline__ void ValuTile<D, BF16, KB>::to_record(const St &s, int lane, unsigned long long *acc_w,
-                                                                unsigned long long *m_w, unsigned long long *l_w,
-                                                                unsigned long long tag) {
-    if (lane < kLpr) {
-#pragma unroll
-        for (int e = 0; e < kEpl; ++e) store_word(acc_w + lane * kEpl + e, tag, s.acc[0][e]);
-    }
-    if (lane == 0) {
-        store_word(m_w, tag, s.m[0]);
-        store_word(l_w, tag, s.l[0]);
-    }
-}
-
-template <int D, int KB>
-__device__ __forceinline__ void MfmaTile<D, KB>::to_record(const St &s, int lane, unsigned long long *acc_w,
-                                                          unsigned long long *m_w, unsigned long long *l_w,
-                                                          unsigned long long tag) {
-    const int n = lane & 15, g = lane >> 4;
-    if (n == 0) {
-#pragma unroll
-        for (int mb = 0; mb < NU; ++mb) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) store_word(acc_w + 16 * mb + 4 * g + i, tag, s.acc[mb][i]);
-        }
-        if (g == 0) {
-            store_word(m_w, tag, s.m);
-            store_word(l_w, tag, s.l);
-        }
-    }
-}
 
 
 // Merger for (b, h) = bh: merges the chunk records of a source with more
@@ -816,26 +753,59 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
     }
 }
 
+// Softmax state of one hypothesis over its generated rows, in the compact
+// layout: m, l in every lane, lane l holding acc for dims l, l + 64, ...
+template <int D>
+struct GenState {
+    static constexpr int kE = (D + kWave - 1) / kWave;
+    float m, l, a[kE];
+};
+
 // Softmax state of hypothesis `hyp` over its own generated rows [0, t) of
 // Kt/Vt for head h (t > 0): the tiles in order, each folded into the running
-// state (beam slot 0 of a one-beam tile).
+// state.  Each tile's state passes through the wave's LDS area (m, l, then
+// acc[D] at float 4), so the running state takes a few registers per lane
+// rather than a whole tile state.
 template <int D, bool BF16>
 __device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                 const uint4 *__restrict__ Vt, size_t hyp, int h, int H, int T,
-                                                int t, int lane, void *lds, float scale_log2,
-                                                typename Tile<D, BF16, 1>::St &st)
+                                                int t, int lane, void *lds, float scale_log2, GenState<D> &gs)
 {
     using TL = Tile<D, BF16, 1>;
-    constexpr int kLpr = Geo<D, BF16>::kLpr, kTile = Geo<D, BF16>::kTile;
+    constexpr int kLpr = Geo<D, BF16>::kLpr, kTile = Geo<D, BF16>::kTile, kE = GenState<D>::kE;
     typename TL::Q qv;
     TL::load_q(qv, q, hyp, h, H, lane);
     const uint4 *Kb = Kt + (hyp * H + h) * (size_t)T * kLpr;
     const uint4 *Vb = Vt + (hyp * H + h) * (size_t)T * kLpr;
-    TL::init(st);
+    float *slot = static_cast<float *>(lds);
+    gs.m = -INFINITY;
+    gs.l = 0.f;
+#pragma unroll
+    for (int e = 0; e < kE; ++e) gs.a[e] = 0.f;
     for (int t0 = 0; t0 < t; t0 += kTile) {
         typename TL::St ts;
         TL::attend(qv, Kb, Vb, t0, t, lane, lds, scale_log2, ts);
-        TL::fold(st, ts);
+        TL::to_lds(ts, lane, slot, slot + 1, slot + 4);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // fold the tile into the running state (the order of merge_state)
+        const float tm = slot[0], tl = slot[1];
+        const float mx = fmaxf(gs.m, tm);
+        const float ms = (mx == -INFINITY) ? 0.f : mx;
+        const float fa = __builtin_amdgcn_exp2f(gs.m - ms);
+        const float fb = __builtin_amdgcn_exp2f(tm - ms);
+        gs.l = gs.l * fa + tl * fb;
+#pragma unroll
+        for (int e = 0; e < kE; ++e) {
+            const int d = lane + e * kWave;
+            if (d < D) gs.a[e] = gs.a[e] * fa + slot[4 + d] * fb;
+        }
+        gs.m = mx;
+        // the next tile's LDS writes stay behind these reads
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 }
 
@@ -848,7 +818,6 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
                                                  int bh, int n_bh, int H, int NC, int T, int t,
                                                  float scale_log2, unsigned long long epoch, void *lds)
 {
-    using TL = Tile<D, BF16, 1>;
     if (bh >= n_bh || t <= 0) return;
     const int b = bh / H;
     const int h = bh - b * H;
@@ -858,9 +827,17 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
     for (int i = w; i < KB; i += kWaves) {
-        typename TL::St st;
-        generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, lds, scale_log2, st);
-        TL::to_record(st, lane, rec + i * D, rec + KB * D + i, rec + KB * D + KB + i, tag);
+        GenState<D> gs;
+        generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, lds, scale_log2, gs);
+#pragma unroll
+        for (int e = 0; e < GenState<D>::kE; ++e) {
+            const int d = lane + e * kWave;
+            if (d < D) store_word(rec + i * D + d, tag, gs.a[e]);
+        }
+        if (lane == 0) {
+            store_word(rec + KB * D + i, tag, gs.m);
+            store_word(rec + KB * D + KB + i, tag, gs.l);
+        }
     }
 }
 
@@ -983,7 +960,6 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
 {
     using G = Geo<D, BF16>;
     using TL = Tile<D, BF16, KB>;
-    using T1 = Tile<D, BF16, 1>;
     constexpr int kLpr = G::kLpr;
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
     constexpr int kW = kWaves * P;                        // waves per workgroup
@@ -1034,10 +1010,18 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
             if constexpr (SPLIT) {
                 // beam i's state over its own generated rows
                 for (int i = wt; i < KB; i += kWaves) {
-                    typename T1::St gst;
+                    GenState<D> gs;
                     generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, &t_lds[w][0],
-                                             scale_log2, gst);
-                    T1::to_lds(gst, lane, &gm_lds[i], &gl_lds[i], &g_lds[i][0]);
+                                             scale_log2, gs);
+#pragma unroll
+                    for (int e = 0; e < GenState<D>::kE; ++e) {
+                        const int d = lane + e * kWave;
+                        if (d < D) g_lds[i][d] = gs.a[e];
+                    }
+                    if (lane == 0) {
+                        gm_lds[i] = gs.m;
+                        gl_lds[i] = gs.l;
+                    }
                 }
             }
         } else if (j0 + cg < njobs) {
@@ -1188,15 +1172,19 @@ AttnPath choose_attn_path(int n_bh, int jobs_max) {
         if (!strcmp(v, "whole2")) return AttnPath::kWhole2;
         if (!strcmp(v, "whole4")) return AttnPath::kWhole4;
     }
-    // Measured on MI355X (bf16, D = 64, k = 4; 192 to 5120 rows of up to
-    // 1024 keys): with four or more rows per CU, one 4-wave workgroup per
-    // row streams at the chip's read rate; with fewer, an 8-wave workgroup
-    // per row (two chunks in flight) beats splitting rows across
-    // workgroups, whose merge costs a round trip through memory.  Only a
-    // few long rows are split.
-    if (jobs_max <= 1 || n_bh >= kWhole1MinRows) return AttnPath::kWhole1;
-    if (n_bh >= kWhole2MinRows || jobs_max <= 2) return AttnPath::kWhole2;
-    return AttnPath::kSplit;
+    // Measured on MI355X (bf16, D = 64, k = 4 or 5; 192 to 5120 rows of up to
+    // 1024 keys): an 8-wave workgroup per row (two jobs in flight) is the
+    // fastest from 256 rows up (BART-shaped 512 rows: 18.6 us against 19.5
+    // for 4 waves; 5120 rows: 128 us against 134); with fewer rows than CUs
+    // a 16-wave workgroup per row uses the idle CUs' share of the row's
+    // jobs (192 rows of the split cache: 12.9 us against 13.9).  Rows of a
+    // single job take 4 waves, and only a few long rows are split across
+    // workgroups, whose merge costs a round trip through memory.
+    if (jobs_max <= 1) return AttnPath::kWhole1;
+    if (jobs_max <= 2) return AttnPath::kWhole2;
+    if (n_bh < kWhole2MinRows) return AttnPath::kSplit;
+    if (n_bh < kCus) return AttnPath::kWhole4;
+    return AttnPath::kWhole2;
 }
 
 int cross_attn_chunk_keys(int D, int esize) {
