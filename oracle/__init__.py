@@ -13,6 +13,9 @@ module only marshals numpy arrays into it:
   per-beam generated-token cache, one softmax over both (Appendix A, Eq. 3).
 * :func:`ngram_block` -- no-repeat-n-gram blocking as its definition
   (Section 4.2, Algorithm 1): ban v iff (last n-1 tokens, v) already occurred.
+* :func:`beam_select` -- one beam-search selection step (Section 2.1): the c
+  best (running score + log-probability) candidates of each source, with the
+  n-gram bans applied to the log-probabilities.
 
 bf16 inputs are passed as their uint16 bit patterns and widened exactly to
 fp64 here (a bf16 value is the upper half of an fp32 value), so the oracle
@@ -46,6 +49,8 @@ def _lib():
         lib.oracle_ngram_block.argtypes = [_ip, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                            ctypes.c_int, _fp, ctypes.c_int]
         lib.oracle_ngram_block.restype = ctypes.c_int
+        lib.oracle_beam_select.argtypes = [_fp, _fp, _ip] + [ctypes.c_int] * 7 + [_dp, _ip, _ip]
+        lib.oracle_beam_select.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
@@ -169,3 +174,37 @@ def ngram_block(tokens, n: int, logits, t: int | None = None) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle_ngram_block rejected its arguments")
     return lg
+
+
+def beam_select(logits, beam_scores, tokens, t: int, n: int, k: int, c: int):
+    """One beam-search selection step (see ``oracle_beam_select`` in oracle.c).
+
+    logits [B*k, V] fp32; beam_scores [B*k] fp32; tokens [B*k, ld] int32 whose
+    first ``t`` columns are the history (ignored, and may be None, when
+    ``n == 0``).  Returns (scores fp64 [B, c], beam int32 [B, c], token int32
+    [B, c]) for every source, best first, equal values in increasing
+    flat index beam*V + token.
+    """
+    lg = np.ascontiguousarray(np.asarray(logits, dtype=np.float32))
+    bs = np.ascontiguousarray(np.asarray(beam_scores, dtype=np.float32))
+    if lg.ndim != 2 or bs.shape != (lg.shape[0],) or k < 1 or lg.shape[0] % k:
+        raise ValueError("logits must be [B*k, V] and beam_scores [B*k]")
+    rows, V = lg.shape
+    B = rows // k
+    if n > 0:
+        tok = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+        if tok.ndim != 2 or tok.shape[0] != rows:
+            raise ValueError("tokens must be [B*k, ld]")
+        ld = tok.shape[1]
+    else:
+        tok = np.zeros((rows, 1), dtype=np.int32)
+        ld, t = 1, 0
+    scores = np.empty((B, c), dtype=np.float64)
+    beam = np.empty((B, c), dtype=np.int32)
+    token = np.empty((B, c), dtype=np.int32)
+    rc = _lib().oracle_beam_select(lg.ctypes.data_as(_fp), bs.ctypes.data_as(_fp), tok.ctypes.data_as(_ip),
+                                   ld, int(t), int(n), B, int(k), V, int(c), scores.ctypes.data_as(_dp),
+                                   beam.ctypes.data_as(_ip), token.ctypes.data_as(_ip))
+    if rc != 0:
+        raise ValueError("oracle_beam_select rejected its arguments")
+    return scores, beam, token

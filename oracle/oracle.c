@@ -18,6 +18,8 @@
  *                       generated-token cache (Appendix A, Eq. 2 and Eq. 3).
  *   oracle_ngram_block  no-repeat-n-gram blocking (Section 4.2, Algorithm 1)
  *                       written as its plain definition.
+ *   oracle_beam_select  one beam-search selection step (Section 2.1) over
+ *                       log-probabilities with the n-gram bans applied.
  */
 #include <math.h>
 #include <stddef.h>
@@ -266,6 +268,128 @@ int oracle_ngram_block(const int32_t *tokens, int ld, int rows, int t, int n,
         }
     }
     return 0;
+}
+
+/*
+ * Tokens banned for one hypothesis by no-repeat-n-gram blocking (Section
+ * 4.2, Algorithm 1, with the readings of oracle_ngram_block): banned[v] = 1
+ * for every v in [0, V) that follows an earlier occurrence of the row's last
+ * n-1 tokens.  n == 0 bans nothing.
+ */
+static void row_bans(const int32_t *x, int t, int n, int V, unsigned char *banned)
+{
+    memset(banned, 0, (size_t)V);
+    if (n < 1 || t < n)
+        return;
+    const int suffix = t - n + 1;
+    for (int j = 0; j <= t - n; ++j) {
+        int same = 1;
+        for (int c = 0; c < n - 1; ++c) {
+            if (x[j + c] != x[suffix + c]) {
+                same = 0;
+                break;
+            }
+        }
+        const int32_t v = x[j + n - 1];
+        if (same && v >= 0 && v < V)
+            banned[v] = 1;
+    }
+}
+
+/*
+ * One beam-search selection step (Section 2.1: at every step beam search
+ * keeps the best candidates of each source), over log-probabilities with
+ * the no-repeat-n-gram bans of Algorithm 1 applied (Section 4.2).
+ *
+ * Source b has hypotheses r = b*k + i (i < k) with running log-probability
+ * beam_scores[r].  With x = logits[r, :]:
+ *   lse_r     = log(sum over every v of exp(x[v]))     (fp64, max subtracted)
+ *   lp(r, v)  = x[v] - lse_r, or -inf if v is banned for row r
+ *               (tokens[r, 0..t-1] with n; n == 0: no bans)
+ *   cand(f)   = beam_scores[r] + lp(r, v),   f = i*V + v
+ * Output for source b: the c largest candidates in descending order, equal
+ * values in increasing f: out_scores[b, j] = cand(f), out_beam[b, j] = i,
+ * out_token[b, j] = v.
+ *
+ * Readings: the normaliser covers every token, banned or not (a ban sets a
+ * log-probability to -inf and does not renormalise the rest); a row whose
+ * logits are all -inf has lp = -inf everywhere; -inf candidates are ordered
+ * like any value (by f), so every c <= k*V is defined.  Logits are finite
+ * or -inf.  The selection is the definition itself: c times, take the best
+ * candidate not taken yet.
+ *
+ * Layouts: logits [B*k, V] fp32, beam_scores [B*k] fp32, tokens [B*k, ld]
+ * int32 (first t columns; not read when n == 0), outputs [B, c].
+ * Returns 0, or 1 for invalid arguments (nothing is written then).
+ */
+int oracle_beam_select(const float *logits, const float *beam_scores, const int32_t *tokens, int ld,
+                       int t, int n, int B, int k, int V, int c,
+                       double *out_scores, int32_t *out_beam, int32_t *out_token)
+{
+    if (B < 0 || k < 0 || V < 0 || c < 0 || n < 0 || (long long)c > (long long)k * V)
+        return 1;
+    if (n > 0 && (t < 0 || ld < t))
+        return 1;
+    if (B == 0 || c == 0)
+        return 0;
+    if (!logits || !beam_scores || (n > 0 && !tokens) || !out_scores || !out_beam || !out_token)
+        return 1;
+    const size_t nc = (size_t)k * V;
+    int bad = 0;
+
+#pragma omp parallel for schedule(dynamic)
+    for (int b = 0; b < B; ++b) {
+        double *cand = malloc(nc * sizeof(double));
+        unsigned char *taken = calloc(nc, 1);
+        unsigned char *banned = malloc((size_t)V > 0 ? (size_t)V : 1);
+        if (!cand || !taken || !banned) {
+#pragma omp atomic write
+            bad = 1;
+            free(cand);
+            free(taken);
+            free(banned);
+            continue;
+        }
+        for (int i = 0; i < k; ++i) {
+            const size_t r = (size_t)b * k + i;
+            const float *x = logits + r * V;
+            double mx = -INFINITY;
+            for (int v = 0; v < V; ++v)
+                if ((double)x[v] > mx)
+                    mx = (double)x[v];
+            double lse = -INFINITY;
+            if (mx > -INFINITY) {
+                double sum = 0.0;
+                for (int v = 0; v < V; ++v)
+                    sum += exp((double)x[v] - mx);
+                lse = mx + log(sum);
+            }
+            row_bans(n > 0 ? tokens + r * ld : NULL, t, n, V, banned);
+            for (int v = 0; v < V; ++v) {
+                double lp = -INFINITY;
+                if (lse > -INFINITY && !banned[v])
+                    lp = (double)x[v] - lse;
+                cand[(size_t)i * V + v] = (double)beam_scores[r] + lp;
+            }
+        }
+        for (int j = 0; j < c; ++j) {
+            size_t best = nc;
+            for (size_t f = 0; f < nc; ++f) {
+                if (taken[f])
+                    continue;
+                if (best == nc || cand[f] > cand[best])
+                    best = f;
+            }
+            taken[best] = 1;
+            out_scores[(size_t)b * c + j] = cand[best];
+            out_beam[(size_t)b * c + j] = (int32_t)(best / (size_t)V);
+            out_token[(size_t)b * c + j] = (int32_t)(best % (size_t)V);
+        }
+        free(cand);
+        free(taken);
+        free(banned);
+    }
+    return bad;
 }
 
 /* Number of OpenMP threads a parallel region of the oracle uses. */
