@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--config", default="bart",
                     help="decode step: tiny | bart | t5 | prophetnet | large; "
                          "split-cache self-attention step: gpt2 | tiny_prefix")
+    ap.add_argument("--part", default="step", choices=("step", "select"),
+                    help="step: the decode step (cross-attention + n-gram blocking); "
+                         "select: the beam-selection step on the same config's logits")
     ap.add_argument("--rounds", type=int, default=5,
                     help="alternating (steps, cross-attention only) region pairs for the per-kernel split")
     ap.add_argument("--rotate-gib", type=float, default=1.0,
@@ -177,6 +180,8 @@ def main() -> int:
     dev = torch.device("cuda:0")
     if args.config in workloads.PREFIX_CONFIGS:
         return bench_prefix(args, workloads.PREFIX_CONFIGS[args.config], dev)
+    if args.part == "select":
+        return bench_select(args, workloads.get(args.config), dev)
     cfg = workloads.get(args.config)
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
 
@@ -413,6 +418,115 @@ def bench_prefix(args, cfg, dev) -> int:
                                 "sample": f"whole {cfg.name}-shaped step, K/V set 0, median of {len(times)} reps, "
                                           f"{sec * 1e3:.1f} ms per step"}
         line["parity"] = {"attn_max_abs_err": err, "attn_tol": tol, "attn_ok": err <= tol}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def select_bytes(rows: int, V: int, t: int, B: int, c: int) -> int:
+    """Algorithmic bytes of one beam-selection call: every logit once, the
+    token history, the beam scores, and the three outputs."""
+    return rows * V * 4 + rows * t * 4 + rows * 4 + B * c * 12
+
+
+def bench_select(args, cfg, dev) -> int:
+    """Beam-selection step (log-softmax, n-gram bans and each source's 2k best
+    candidates) over the decode-step config's logits.  A step is one
+    fs_beam_select call; each reads a different logits set, rotating over at
+    least 1 GiB."""
+    import numpy as np
+    import torch
+
+    from paper_2106_04718_amd import api, workloads
+
+    t0 = time.perf_counter()
+    d = workloads.select_inputs(cfg)
+    rows, V, k, c, B = cfg.rows, cfg.V, d["k"], d["c"], d["B"]
+    set_bytes = rows * V * 4
+    R = max(1, math.ceil(args.rotate_gib * (1 << 30) / set_bytes))
+    lg0 = torch.from_numpy(d["logits"]).to(dev)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(210604718 + cfg.index)
+    sets = [lg0] + [torch.randn(rows, V, generator=gen, device=dev, dtype=torch.float32) for _ in range(R - 1)]
+    bs = torch.from_numpy(d["beam_scores"]).to(dev)
+    tok = torch.from_numpy(d["tokens"]).to(dev)
+    outs = (torch.empty((B, c), dtype=torch.float32, device=dev), torch.empty((B, c), dtype=torch.int32, device=dev),
+            torch.empty((B, c), dtype=torch.int32, device=dev))
+    ws = api.new_workspace(api.beam_select_workspace_bytes(B, k, V, c), dev)
+    torch.cuda.synchronize()
+    log(f"config={cfg.name} select: logits sets={R} ({R * set_bytes / 2**30:.2f} GiB) inputs ready in "
+        f"{time.perf_counter() - t0:.1f}s")
+
+    def step(i: int):
+        api.beam_select(sets[i % R], bs, k, c, tokens=tok, n=cfg.n, out=outs, workspace=ws)
+
+    step(0)
+    torch.cuda.synchronize()
+    first = tuple(o.cpu().numpy().copy() for o in outs)
+    for i in range(args.warmup):
+        step(i)
+    K_ = args.steps
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(K_):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / K_
+    spread = launch_spread(stream, step, K_)
+    b = select_bytes(rows, V, cfg.t, B, c)
+    gbps = b / (us * 1e-6) / 1e9
+    copy_gbps = copy_bandwidth(dev)
+    log(f"select step {us:.2f} us = {gbps:.0f} GB/s ({100 * gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
+        f"{100 * gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s)")
+    line = {
+        "metric": "beam-selection step µs and achieved HBM GB/s (log-softmax + n-gram ban + per-source top-2k)",
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K_,
+        "warmup": args.warmup,
+        "ms_per_step": round(us * 1e-3, 6),
+        "step_us": round(us, 3),
+        "step_us_spread": spread,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded; N(0,1) logits, Zipf token prefixes with one planted repeat per row)",
+        "config": {"workload": (f"{cfg.name}-shaped beam-selection step: {rows} hypotheses (B={B}, k={k}) x "
+                                f"V={V} fp32 logits, no-repeat-{cfg.n}-gram on t={cfg.t} tokens, c={c} "
+                                f"candidates per source"),
+                   "B": B, "k": k, "V": V, "t": cfg.t, "n": cfg.n, "c": c, "logits_sets_rotated": R,
+                   "bytes_per_step": b},
+        "copy_gbps": round(copy_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": "fs_beam_select", "achieved": round(gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "algorithmic_bytes_per_launch": b,
+                     "traffic": load_traffic(args.traffic, cfg.name + "-select")},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        times, ref = [], None
+        while True:
+            c0 = time.perf_counter()
+            ref = oracle.beam_select(d["logits"], d["beam_scores"], d["tokens"], cfg.t, cfg.n, k, c)
+            times.append(time.perf_counter() - c0)
+            if (args.cpu_reps and len(times) >= args.cpu_reps) or \
+                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                break
+        sec = float(np.median(times))
+        same = bool(np.array_equal(first[1], ref[1]) and np.array_equal(first[2], ref[2]))
+        err = float(np.max(np.abs(first[0].astype(np.float64) - ref[0])))
+        log(f"oracle: {sec * 1e3:.1f} ms per step on {oracle.num_threads()} threads; same picks {same}, "
+            f"max score err {err:.2e}")
+        line["cpu_baseline"] = {"value": round(b / sec / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
+                                "kind": "oracle",
+                                "sample": f"whole {cfg.name}-shaped selection step, logits set 0, median of "
+                                          f"{len(times)} reps, {sec * 1e3:.1f} ms per step"}
+        line["parity"] = {"same_picks": same, "max_score_err": err}
     print(json.dumps(line), flush=True)
     return 0
 

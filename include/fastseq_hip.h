@@ -10,6 +10,12 @@
  *   fs_ngram_block      no-repeat-n-gram blocking on the GPU (Section 4.2,
  *                       Algorithm 1): logits of tokens that would repeat an
  *                       earlier n-gram become -inf, in place.
+ *   fs_beam_prefix_attn self-attention over a split cache: the prefix shared
+ *                       by a sample's beams is stored once (Section 4.1.1;
+ *                       Appendix A, Eq. 2-3).
+ *   fs_beam_select      one beam-search selection step (Section 2.1): the n-gram
+ *                       bans, the log-softmax and each source's best
+ *                       candidates in one pass over the logits.
  *
  * Conventions shared by every entry point
  *   - Pointers named "device" are HIP device memory; the caller owns every
@@ -185,6 +191,63 @@ int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int
  */
 int fs_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t, int n,
                    float *logits, int V, void *stream);
+
+/*
+ * Workspace, in bytes, that fs_beam_select needs for these sizes (per
+ * (hypothesis, vocabulary slice) partial records).  Zero-fill it before its
+ * first use; the reuse rules are those of fs_beam_cross_attn's workspace.
+ * 0 for empty problems; (size_t)-1 for invalid or unsupported sizes.
+ */
+size_t fs_beam_select_workspace_bytes(int B, int k, int V, int c);
+
+/*
+ * One beam-search selection step (Section 2.1: at every step beam search
+ * keeps the best candidates of each source) with the no-repeat-n-gram bans
+ * of Section 4.2, Algorithm 1, in one pass over the logits.
+ *
+ * Source b has hypotheses r = b*k + i (i < k) with running log-probabilities
+ * beam_scores[r].  With x = logits[r, :]:
+ *     lse_r      = log(sum over every v of exp(x[v]))
+ *     cand(i*V+v) = beam_scores[r] + x[v] - lse_r, or -inf if v is banned for
+ *                   row r (the rule of fs_ngram_block on tokens[r, 0..t-1])
+ * and out_*[b, 0..c-1] are the c largest candidates of source b, best first,
+ * equal values in increasing flat index i*V + v: out_scores the value,
+ * out_beam the beam i, out_token the token v.  The normaliser covers every
+ * token, banned or not (a ban sets a log-probability to -inf and does not
+ * renormalise the rest).  A row whose logits are all -inf has -inf
+ * candidates; -inf candidates are ordered by flat index like any value.
+ *
+ * Arguments (device pointers except the sizes):
+ *   logits       [B*k, V] fp32, finite or -inf; read once, never written
+ *   beam_scores  [B*k]    fp32
+ *   tokens       [B*k, ld_tokens] int32, columns 0..t-1; not read if n == 0
+ *   t, n         history length and n-gram size; n == 0 bans nothing
+ *   out_scores   [B, c] fp32;  out_beam, out_token [B, c] int32
+ *   workspace, workspace_bytes  at least fs_beam_select_workspace_bytes
+ *                bytes, zero-filled before its first use
+ *   stream       hipStream_t (NULL = default stream)
+ * Supported: 1 <= c <= 16 and c <= k*V, 1 <= k <= 16, V >= 1, and for one
+ * source at most 1024 candidates in the final ranking (k * c * slices, where
+ * a row is cut into slices of at most 16381 logits) and 2048 partial-record
+ * words (k * slices * (2 + 2c)); the slice count is reduced to fit these
+ * when it can be, so only a vocabulary above 16381 * (1024 / (k * c))
+ * logits can exceed them.  The slice count follows from the sizes;
+ * FS_SELECT_SLICES (read once per process) sets it within the same limits.
+ * Arithmetic: fp32 (the normaliser from per-slice maxima and sums of exp);
+ * the order and the bits of the result depend on the data, the slice count
+ * and the address of logits modulo 16 bytes, never on run or launch.
+ * Errors: FS_ERR_INVALID_ARG for null pointers with non-empty sizes, negative
+ * sizes, n < 0, ld_tokens < t with n > 0, c > k*V, pointers not 4-byte
+ * aligned, a workspace that is too small, or an output overlapping an input
+ * or another output; FS_ERR_UNSUPPORTED for c, k or the candidate count
+ * outside the set above; FS_ERR_HIP for a failed launch.  B == 0 returns
+ * FS_OK with no launch.  If a partial record is not seen within about 10 ms
+ * (which does not happen in a working launch), the source's outputs are NaN
+ * and -1.
+ */
+int fs_beam_select(const float *logits, const float *beam_scores, const int32_t *tokens, int ld_tokens,
+                   int t, int n, float *out_scores, int32_t *out_beam, int32_t *out_token,
+                   int B, int k, int V, int c, void *workspace, size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

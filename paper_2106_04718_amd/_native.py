@@ -34,6 +34,9 @@ SIGNATURES = [
     ("fs_beam_prefix_attn", _c_int,
      [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
     ("fs_ngram_block", _c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp]),
+    ("fs_beam_select_workspace_bytes", _c_size, [_c_int] * 4),
+    ("fs_beam_select", _c_int,
+     [_vp, _vp, _vp, _c_int, _c_int, _c_int, _vp, _vp, _vp] + [_c_int] * 4 + [_vp, _c_size, _vp]),
 ]
 
 _lib = None

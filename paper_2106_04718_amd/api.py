@@ -199,3 +199,71 @@ def ngram_block(tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | Non
         _N.check(_N.ext().fs_ngram_block(tokens.data_ptr(), ld, rows, int(t), int(n),
                                          logits.data_ptr(), logits.shape[1], _stream_ptr(dev)))
     return logits
+
+
+def beam_select_workspace_bytes(B: int, k: int, V: int, c: int) -> int:
+    """Bytes of workspace fs_beam_select needs for these sizes."""
+    key = ("s", B, k, V, c)
+    n = _WS_BYTES.get(key)
+    if n is None:
+        n = _size_or_raise(_native_lib().fs_beam_select_workspace_bytes(B, k, V, c))
+        _WS_BYTES[key] = n
+    return n
+
+
+def beam_select(logits: torch.Tensor, beam_scores: torch.Tensor, k: int, c: int,
+                tokens: torch.Tensor | None = None, n: int = 0, t: int | None = None,
+                out: tuple | None = None, workspace: torch.Tensor | None = None):
+    """One beam-search selection step (Section 2.1) with no-repeat-n-gram bans
+    (Section 4.2, Algorithm 1), in one pass over the logits.
+
+    logits [B*k, V] float32 (not modified); beam_scores [B*k] float32;
+    tokens [B*k, ld] int32 whose first ``t`` columns (default all) are the
+    history, required when ``n > 0``.  Returns (scores float32 [B, c],
+    beam int32 [B, c], token int32 [B, c]): each source's c best
+    beam_score + log-softmax candidates, best first, ties to the smaller
+    flat index beam*V + token.  ``out`` may pass the three output tensors.
+    """
+    _need_cuda("logits", logits)
+    _need_cuda("beam_scores", beam_scores)
+    if logits.dim() != 2 or logits.dtype != torch.float32:
+        raise ValueError("logits must be float32 [B*k, V]")
+    rows, V = logits.shape
+    if k < 1 or rows % k:
+        raise ValueError(f"rows={rows} is not a multiple of k={k}")
+    B = rows // k
+    dev = logits.device
+    if beam_scores.dtype != torch.float32 or beam_scores.shape != (rows,) or beam_scores.device != dev:
+        raise ValueError("beam_scores must be float32 [B*k] on the logits' device")
+    ld, tp, tptr = 0, 0, 0
+    if n > 0:
+        if not isinstance(tokens, torch.Tensor) or tokens.device != dev:
+            raise ValueError("tokens must be a GPU tensor on the logits' device when n > 0")
+        if tokens.dim() != 2 or tokens.dtype != torch.int32 or tokens.shape[0] != rows:
+            raise ValueError("tokens must be int32 [B*k, ld]")
+        if rows > 0 and tokens.shape[1] > 1 and tokens.stride(1) != 1:
+            raise ValueError("tokens must have unit column stride")
+        ld = tokens.stride(0) if rows > 1 else tokens.shape[1]
+        tp = tokens.shape[1] if t is None else int(t)
+        if tp > tokens.shape[1]:
+            raise ValueError("t exceeds the columns of tokens")
+        tptr = tokens.data_ptr()
+    if out is None:
+        out = (torch.empty((B, c), dtype=torch.float32, device=dev),
+               torch.empty((B, c), dtype=torch.int32, device=dev),
+               torch.empty((B, c), dtype=torch.int32, device=dev))
+    else:
+        for o, dt in zip(out, (torch.float32, torch.int32, torch.int32)):
+            _need_cuda("out", o)
+            if o.shape != (B, c) or o.dtype != dt or o.device != dev:
+                raise ValueError("out must be (float32, int32, int32) tensors of shape [B, c]")
+    if workspace is None:
+        workspace = new_workspace(beam_select_workspace_bytes(B, k, V, c), dev)
+    else:
+        _need_cuda("workspace", workspace)
+    with _on(dev):
+        _N.check(_N.ext().fs_beam_select(
+            logits.data_ptr(), beam_scores.data_ptr(), tptr, ld, tp, int(n), out[0].data_ptr(),
+            out[1].data_ptr(), out[2].data_ptr(), B, int(k), V, int(c), workspace.data_ptr(),
+            workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
+    return out

@@ -252,3 +252,87 @@ int fs_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t, int n,
 }
 
 }  // extern "C"
+
+namespace {
+
+int check_select_sizes(int B, int k, int V, int c) {
+    if (B < 0 || k < 0 || V < 0 || c < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (B=%d k=%d V=%d c=%d)", B, k, V, c);
+    if (k < 1 || k > 16) return fail(FS_ERR_UNSUPPORTED, "beam size k=%d outside [1, 16]", k);
+    if (V < 1) return fail(FS_ERR_INVALID_ARG, "vocabulary V=%d < 1", V);
+    if (c < 1 || c > 16) return fail(FS_ERR_UNSUPPORTED, "c=%d outside [1, 16]", c);
+    if ((long long)c > (long long)k * V) return fail(FS_ERR_INVALID_ARG, "c=%d > k*V=%lld", c, (long long)k * V);
+    if ((long long)k * V > 0xffffffffLL) return fail(FS_ERR_UNSUPPORTED, "k*V=%lld flat indices exceed 32 bits",
+                                                     (long long)k * V);
+    const long long rows = (long long)B * k;
+    if (rows > INT_MAX) return fail(FS_ERR_INVALID_ARG, "B*k=%lld too large", rows);
+    const int ns = fs::beam_select_slices((int)rows, V, k, c);
+    if ((long long)k * ns * c > fs::beam_select_max_candidates())
+        return fail(FS_ERR_UNSUPPORTED, "k*slices*c=%lld candidates per source exceed %d", (long long)k * ns * c,
+                    fs::beam_select_max_candidates());
+    if ((long long)k * ns * (2 + 2 * c) > fs::beam_select_max_record_words())
+        return fail(FS_ERR_UNSUPPORTED, "k*slices*(2+2c)=%lld record words per source exceed %d",
+                    (long long)k * ns * (2 + 2 * c), fs::beam_select_max_record_words());
+    if (rows * ns + B > INT_MAX) return fail(FS_ERR_INVALID_ARG, "problem too large for one launch");
+    return FS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t fs_beam_select_workspace_bytes(int B, int k, int V, int c) {
+    g_last_error.clear();
+    if (check_select_sizes(B, k, V, c) != FS_OK) return (size_t)-1;
+    if (B == 0) return 0;
+    return fs::beam_select_workspace_words(B, k, V, c) * 8;
+}
+
+int fs_beam_select(const float *logits, const float *beam_scores, const int32_t *tokens, int ld_tokens,
+                   int t, int n, float *out_scores, int32_t *out_beam, int32_t *out_token,
+                   int B, int k, int V, int c, void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_last_error.clear();
+    int st = check_select_sizes(B, k, V, c);
+    if (st != FS_OK) return st;
+    if (n < 0 || t < 0 || ld_tokens < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (n=%d t=%d ld_tokens=%d)", n, t, ld_tokens);
+    if (n > 0 && ld_tokens < t) return fail(FS_ERR_INVALID_ARG, "ld_tokens=%d < t=%d", ld_tokens, t);
+    if (B == 0) return FS_OK;
+    const bool need_tokens = n > 0 && t >= n;
+    if (!logits || !beam_scores || !out_scores || !out_beam || !out_token || (need_tokens && !tokens))
+        return fail(FS_ERR_INVALID_ARG, "null pointer (logits=%p beam_scores=%p tokens=%p outputs=%p %p %p)",
+                    (const void *)logits, (const void *)beam_scores, (const void *)tokens, (void *)out_scores,
+                    (void *)out_beam, (void *)out_token);
+    if (!aligned(logits, 4) || !aligned(beam_scores, 4) || !aligned(tokens, 4) || !aligned(out_scores, 4) ||
+        !aligned(out_beam, 4) || !aligned(out_token, 4))
+        return fail(FS_ERR_INVALID_ARG, "arrays must be 4-byte aligned");
+    const size_t rows = (size_t)B * k;
+    const size_t lg_bytes = rows * V * 4, bs_bytes = rows * 4, o_bytes = (size_t)B * c * 4;
+    const size_t tok_bytes = need_tokens ? ((rows - 1) * ld_tokens + t) * 4 : 0;
+    const void *outs[3] = {out_scores, out_beam, out_token};
+    for (int i = 0; i < 3; ++i) {
+        if (overlaps(outs[i], o_bytes, logits, lg_bytes) || overlaps(outs[i], o_bytes, beam_scores, bs_bytes) ||
+            overlaps(outs[i], o_bytes, tokens, tok_bytes))
+            return fail(FS_ERR_INVALID_ARG, "an output overlaps an input");
+        for (int j = i + 1; j < 3; ++j)
+            if (overlaps(outs[i], o_bytes, outs[j], o_bytes)) return fail(FS_ERR_INVALID_ARG, "outputs overlap");
+    }
+    const size_t need = fs_beam_select_workspace_bytes(B, k, V, c);
+    if (workspace_bytes < need || !workspace)
+        return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed", workspace_bytes,
+                    workspace, need);
+    if (!aligned(workspace, 16)) return fail(FS_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (overlaps(workspace, need, logits, lg_bytes) || overlaps(workspace, need, beam_scores, bs_bytes) ||
+        overlaps(workspace, need, tokens, tok_bytes) || overlaps(workspace, need, out_scores, o_bytes) ||
+        overlaps(workspace, need, out_beam, o_bytes) || overlaps(workspace, need, out_token, o_bytes))
+        return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
+    hipError_t e = fs::launch_beam_select(logits, beam_scores, need_tokens ? tokens : nullptr, ld_tokens, t,
+                                          need_tokens ? n : 0, out_scores, out_beam, out_token, B, k, V, c,
+                                          static_cast<unsigned long long *>(workspace), next_epoch(),
+                                          static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "fs_beam_select launch");
+    return FS_OK;
+}
+
+}  // extern "C"

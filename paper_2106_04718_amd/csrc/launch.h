@@ -49,4 +49,16 @@ hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, con
 hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t,
                               int n, float *logits, int V, hipStream_t stream);
 
+// Beam selection: vocabulary slices per hypothesis row, the most candidates
+// one source's ranking takes (k * slices * c) and the most record words it
+// reads (k * slices * (2 + 2c)), and the workspace in 64-bit words.  Record words carry the low 32 bits of `epoch` as their tag.
+int beam_select_slices(int rows, int V, int k, int c);
+int beam_select_max_candidates();
+int beam_select_max_record_words();
+size_t beam_select_workspace_words(int B, int k, int V, int c);
+hipError_t launch_beam_select(const float *logits, const float *beam_scores, const int32_t *tokens, int ld,
+                              int t, int n, float *out_scores, int32_t *out_beam, int32_t *out_token, int B,
+                              int k, int V, int c, unsigned long long *workspace, unsigned long long epoch,
+                              hipStream_t stream);
+
 }  // namespace fs

@@ -75,6 +75,17 @@ static PyObject *py_ngram_block(PyObject *self, PyObject *const *args, Py_ssize_
     return PyLong_FromLong(st);
 }
 
+static PyObject *py_beam_select(PyObject *self, PyObject *const *args, Py_ssize_t nargs) {
+    unsigned long long u[16];
+    int v[16];
+    (void)self;
+    if (unpack(args, nargs, "pppiiipppiiiippp", u, v)) return NULL;
+    int st = fs_beam_select((const float *)PTR(0), (const float *)PTR(1), (const int32_t *)PTR(2), v[3], v[4],
+                            v[5], (float *)PTR(6), (int32_t *)PTR(7), (int32_t *)PTR(8), v[9], v[10], v[11],
+                            v[12], PTR(13), (size_t)u[14], PTR(15));
+    return PyLong_FromLong(st);
+}
+
 static PyObject *py_last_error(PyObject *self, PyObject *unused) {
     (void)self;
     (void)unused;
@@ -89,6 +100,9 @@ static PyMethodDef methods[] = {
      "workspace_bytes, stream)"},
     {"fs_ngram_block", (PyCFunction)(void (*)(void))py_ngram_block, METH_FASTCALL,
      "fs_ngram_block(tokens, ld_tokens, rows, t, n, logits, V, stream)"},
+    {"fs_beam_select", (PyCFunction)(void (*)(void))py_beam_select, METH_FASTCALL,
+     "fs_beam_select(logits, beam_scores, tokens, ld_tokens, t, n, out_scores, out_beam, out_token, B, k, V, c, "
+     "workspace, workspace_bytes, stream)"},
     {"fs_last_error", py_last_error, METH_NOARGS, "fs_last_error() -> str"},
     {NULL, NULL, 0, NULL},
 };

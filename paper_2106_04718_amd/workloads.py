@@ -269,3 +269,24 @@ def low_entropy_rows(rows: int, t: int, rng) -> np.ndarray:
         else:
             out[r] = rng.integers(0, 2 + (kind - 2), size=t)
     return out
+
+
+def select_inputs(cfg, planted: int = 1) -> dict:
+    """Inputs of one beam-selection step on a decode-step config.
+
+    logits and tokens are those of :func:`ngram_inputs`; every row also gets
+    ``planted`` copies of its trailing n-1 tokens (so that bans occur on the
+    Zipf data, which rarely repeats an n-gram by itself).  beam_scores are the
+    running log-probabilities of the k hypotheses of each source: per source,
+    k draws of -|N(0, 1)| * 2 - 10 sorted best first, from the seed stream
+    SeedSequence([210604718, cfg, 1000]) (apart from the K/V rotation sets,
+    which use small third keys).  c = 2k candidates are kept.
+    """
+    cfg = get(cfg)
+    d = ngram_inputs(cfg)
+    rng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, cfg.index, 1000]))
+    tokens = plant_repeats(d["tokens"], cfg.n, cfg.t, rng, per_row=planted) if planted else d["tokens"]
+    bs = -np.abs(rng.standard_normal(size=(cfg.B, cfg.k))) * 2.0 - 10.0
+    bs = -np.sort(-bs, axis=1)
+    return {"logits": d["logits"], "tokens": tokens, "beam_scores": bs.astype(np.float32).reshape(-1),
+            "n": cfg.n, "t": cfg.t, "k": cfg.k, "c": 2 * cfg.k, "B": cfg.B, "V": cfg.V}
