@@ -16,6 +16,9 @@ module only marshals numpy arrays into it:
 * :func:`beam_select` -- one beam-search selection step (Section 2.1): the c
   best (running score + log-probability) candidates of each source, with the
   n-gram bans applied to the log-probabilities.
+* :func:`cache_reorder` -- the per-beam cache reorder after a selection step
+  (Section 2.2 cache maintenance, Section 4.1.1): each new hypothesis takes
+  its parent's generated-token cache.
 
 bf16 inputs are passed as their uint16 bit patterns and widened exactly to
 fp64 here (a bf16 value is the upper half of an fp32 value), so the oracle
@@ -51,6 +54,8 @@ def _lib():
         lib.oracle_ngram_block.restype = ctypes.c_int
         lib.oracle_beam_select.argtypes = [_fp, _fp, _ip] + [ctypes.c_int] * 7 + [_dp, _ip, _ip]
         lib.oracle_beam_select.restype = ctypes.c_int
+        lib.oracle_cache_reorder.argtypes = [ctypes.c_void_p, _ip] + [ctypes.c_int] * 7
+        lib.oracle_cache_reorder.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
@@ -208,3 +213,24 @@ def beam_select(logits, beam_scores, tokens, t: int, n: int, k: int, c: int):
     if rc != 0:
         raise ValueError("oracle_beam_select rejected its arguments")
     return scores, beam, token
+
+
+def cache_reorder(cache, parent, k: int, t: int) -> np.ndarray:
+    """Per-beam cache reorder (see ``oracle_cache_reorder`` in oracle.c).
+
+    cache [B*k, H, T, D] of any fixed-size dtype (bf16 as uint16 bits);
+    parent [B*k] int32, the old beam each new hypothesis continues.  Returns
+    the reordered copy: rows tau < t of hypothesis b*k + j become those of
+    b*k + parent[b*k + j]; other rows, and rows with a parent outside
+    [0, k), keep their bytes.
+    """
+    x = np.array(cache, copy=True, order="C")
+    par = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    if x.ndim != 4 or k < 1 or x.shape[0] % k or par.shape != (x.shape[0],):
+        raise ValueError("cache must be [B*k, H, T, D] and parent [B*k]")
+    rows, H, T, D = x.shape
+    rc = _lib().oracle_cache_reorder(x.ctypes.data_as(ctypes.c_void_p), par.ctypes.data_as(_ip), rows // k, int(k),
+                                     H, T, int(t), D, x.dtype.itemsize)
+    if rc != 0:
+        raise ValueError("oracle_cache_reorder rejected its arguments")
+    return x

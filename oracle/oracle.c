@@ -20,6 +20,8 @@
  *                       written as its plain definition.
  *   oracle_beam_select  one beam-search selection step (Section 2.1) over
  *                       log-probabilities with the n-gram bans applied.
+ *   oracle_cache_reorder the per-beam cache reorder that follows a selection
+ *                       step (Section 2.2, cache maintenance; Section 4.1.1).
  */
 #include <math.h>
 #include <stddef.h>
@@ -388,6 +390,60 @@ int oracle_beam_select(const float *logits, const float *beam_scores, const int3
         free(cand);
         free(taken);
         free(banned);
+    }
+    return bad;
+}
+
+/*
+ * Per-beam cache reorder after a selection step (Section 2.2, cache
+ * maintenance; Section 4.1.1: with the cache split, only the per-beam part
+ * Cache_K_t / Cache_V_t is reordered, the shared prefix never is).
+ *
+ * Beam search keeps k hypotheses per source; the new hypothesis j of source b
+ * continues the old hypothesis parent[b*k + j] of the same source, so its
+ * cache of generated tokens must hold what that parent's held.  For every
+ * source b, beam j, head h and position tau < t:
+ *     new[b*k + j, h, tau, :] = old[b*k + parent[b*k + j], h, tau, :]
+ * Positions tau >= t (unused capacity) keep their bytes.  A parent outside
+ * [0, k) leaves the row as it is (the hypothesis keeps its own history).
+ *
+ * The cache is raw bytes, esize bytes per element, [B*k, H, T, D] row-major;
+ * it is rewritten in place from a copy of each source's old rows, so the
+ * result does not depend on the order of the copies.
+ * Returns 0, or 1 for invalid arguments (nothing is written then).
+ */
+int oracle_cache_reorder(unsigned char *cache, const int32_t *parent, int B, int k, int H, int T, int t, int D,
+                         int esize)
+{
+    if (B < 0 || k < 1 || H < 0 || T < 0 || t < 0 || t > T || D < 0 || esize < 1)
+        return 1;
+    if ((long long)B * k * H * T * D == 0 || t == 0)
+        return 0;
+    if (!cache || !parent)
+        return 1;
+    const size_t row = (size_t)D * esize;              /* bytes of one (h, tau) vector */
+    const size_t beam = (size_t)H * T * row;            /* bytes of one hypothesis */
+    int bad = 0;
+
+#pragma omp parallel for schedule(static)
+    for (int b = 0; b < B; ++b) {
+        unsigned char *src = cache + (size_t)b * k * beam;
+        unsigned char *old = malloc((size_t)k * beam);
+        if (!old) {
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        memcpy(old, src, (size_t)k * beam);
+        for (int j = 0; j < k; ++j) {
+            const int32_t pj = parent[(size_t)b * k + j];
+            const int from = (pj >= 0 && pj < k) ? pj : j;
+            for (int h = 0; h < H; ++h)
+                for (int tau = 0; tau < t; ++tau)
+                    memcpy(src + (size_t)j * beam + ((size_t)h * T + tau) * row,
+                           old + (size_t)from * beam + ((size_t)h * T + tau) * row, row);
+        }
+        free(old);
     }
     return bad;
 }
