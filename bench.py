@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--config", default="bart",
                     help="decode step: tiny | bart | t5 | prophetnet | large; "
                          "split-cache self-attention step: gpt2 | tiny_prefix")
-    ap.add_argument("--part", default="step", choices=("step", "select"),
+    ap.add_argument("--part", default="step", choices=("step", "select", "reorder"),
                     help="step: the decode step (cross-attention + n-gram blocking); "
                          "select: the beam-selection step on the same config's logits")
     ap.add_argument("--rounds", type=int, default=5,
@@ -182,6 +182,8 @@ def main() -> int:
         return bench_prefix(args, workloads.PREFIX_CONFIGS[args.config], dev)
     if args.part == "select":
         return bench_select(args, workloads.get(args.config), dev)
+    if args.part == "reorder":
+        return bench_reorder(args, workloads.get(args.config), dev)
     cfg = workloads.get(args.config)
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
 
@@ -535,6 +537,122 @@ def workload_name(cfg) -> str:
     return (f"{cfg.name}-shaped decode step: cross-attn B={cfg.B} k={cfg.k} H={cfg.H} D={cfg.D} "
             f"S={cfg.S} (lengths U{{{cfg.len_lo}..{cfg.len_hi}}}) {cfg.dtype} + no-repeat-{cfg.n}-gram "
             f"on [{cfg.rows}, {cfg.t}] tokens, V={cfg.V}")
+
+
+def reorder_bytes(parent, k: int, row_bytes: int, tensors: int = 2) -> int:
+    """Algorithmic bytes of one cache reorder: each beam some other beam of
+    its source continues is read once, each beam whose parent is another
+    beam is written once; row_bytes = H*t*D*esize per beam and tensor."""
+    import numpy as np
+    p = np.asarray(parent).reshape(-1, k)
+    reads = writes = 0
+    for row in p:
+        moved = [j for j in range(k) if 0 <= row[j] < k and row[j] != j]
+        writes += len(moved)
+        reads += len({int(row[j]) for j in moved})
+    return (reads + writes) * row_bytes * tensors
+
+
+def bench_reorder(args, cfg, dev) -> int:
+    """Per-beam cache reorder of one decoder layer's K and V on the
+    decode-step config.  A step is one fs_cache_reorder call; each reorders a
+    different cache set, rotating over at least 1 GiB."""
+    import numpy as np
+    import torch
+
+    from paper_2106_04718_amd import api, workloads
+
+    t0 = time.perf_counter()
+    d = workloads.reorder_inputs(cfg)
+    B, k, H, T, t, D = d["B"], d["k"], d["H"], d["T"], d["t"], d["D"]
+    dt = torch.bfloat16 if d["dtype"] == "bf16" else torch.float32
+    esize = 2 if dt == torch.bfloat16 else 4
+    set_bytes = 2 * B * k * H * T * D * esize
+    R = max(1, math.ceil(args.rotate_gib * (1 << 30) / set_bytes))
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(210604718 + cfg.index)
+    sets = [(torch.randn((B * k, H, T, D), generator=gen, device=dev).to(dt),
+             torch.randn((B * k, H, T, D), generator=gen, device=dev).to(dt)) for _ in range(R)]
+    parent = torch.from_numpy(d["parent"]).to(dev)
+    b = reorder_bytes(d["parent"], k, H * t * D * esize)
+    torch.cuda.synchronize()
+    log(f"config={cfg.name} reorder: cache sets={R} ({R * set_bytes / 2**30:.2f} GiB), "
+        f"{b / 1e6:.1f} MB moved per call, inputs ready in {time.perf_counter() - t0:.1f}s")
+
+    def step(i: int):
+        Kc, Vc = sets[i % R]
+        api.cache_reorder(Kc, Vc, parent, k, t)
+
+    for i in range(args.warmup):
+        step(i)
+    K_ = args.steps
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(K_):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / K_
+    spread = launch_spread(stream, step, K_)
+    gbps = b / (us * 1e-6) / 1e9
+    copy_gbps = copy_bandwidth(dev)
+    log(f"reorder step {us:.2f} us = {gbps:.0f} GB/s ({100 * gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
+        f"{100 * gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s)")
+    line = {
+        "metric": "per-beam cache reorder µs and achieved HBM GB/s (one decoder layer's K and V, in place)",
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K_,
+        "warmup": args.warmup,
+        "ms_per_step": round(us * 1e-3, 6),
+        "step_us": round(us, 3),
+        "step_us_spread": spread,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": d["dtype"],
+        "data": "synthetic (seeded; N(0,1) cache values, parents floor(k*u^2))",
+        "config": {"workload": (f"{cfg.name}-shaped per-beam cache reorder: K and V [{B * k}, {H}, {T}, {D}] "
+                                f"{d['dtype']} (B={B}, k={k}), t={t} positions, seeded parents"),
+                   "B": B, "k": k, "H": H, "T": T, "t": t, "D": D, "cache_sets_rotated": R,
+                   "bytes_per_step": b},
+        "copy_gbps": round(copy_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": "fs_cache_reorder", "achieved": round(gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "algorithmic_bytes_per_launch": b,
+                     "traffic": load_traffic(args.traffic, cfg.name + "-reorder")},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        Kc, Vc = sets[0]
+        view = torch.int16 if dt == torch.bfloat16 else torch.int32
+        kh, vh = Kc.view(view).cpu().numpy(), Vc.view(view).cpu().numpy()
+        par = d["parent"]
+        times = []
+        while True:
+            c0 = time.perf_counter()
+            rk = oracle.cache_reorder(kh, par, k, t)
+            rv = oracle.cache_reorder(vh, par, k, t)
+            times.append(time.perf_counter() - c0)
+            if (args.cpu_reps and len(times) >= args.cpu_reps) or \
+                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                break
+        sec = float(np.median(times))
+        api.cache_reorder(Kc, Vc, parent, k, t)
+        torch.cuda.synchronize()
+        same = bool(np.array_equal(Kc.view(view).cpu().numpy(), rk) and np.array_equal(Vc.view(view).cpu().numpy(), rv))
+        log(f"oracle: {sec * 1e3:.1f} ms per step on {oracle.num_threads()} threads; GPU bit-exact {same}")
+        line["cpu_baseline"] = {"value": round(b / sec / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
+                                "kind": "oracle",
+                                "sample": f"whole {cfg.name}-shaped reorder step (K and V), cache set 0, median of "
+                                          f"{len(times)} reps, {sec * 1e3:.1f} ms per step"}
+        line["parity"] = {"bit_exact": same}
+    print(json.dumps(line), flush=True)
+    return 0
 
 
 def kernel_source_sha() -> str:

@@ -16,6 +16,9 @@
  *   fs_beam_select      one beam-search selection step (Section 2.1): the n-gram
  *                       bans, the log-softmax and each source's best
  *                       candidates in one pass over the logits.
+ *   fs_cache_reorder    the per-beam cache reorder after a selection step
+ *                       (Section 2.2, cache maintenance; Section 4.1.1), in
+ *                       place.
  *
  * Conventions shared by every entry point
  *   - Pointers named "device" are HIP device memory; the caller owns every
@@ -248,6 +251,39 @@ size_t fs_beam_select_workspace_bytes(int B, int k, int V, int c);
 int fs_beam_select(const float *logits, const float *beam_scores, const int32_t *tokens, int ld_tokens,
                    int t, int n, float *out_scores, int32_t *out_beam, int32_t *out_token,
                    int B, int k, int V, int c, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Per-beam cache reorder after a selection step (Section 2.2: beam search
+ * reorders the cached keys and values of the kept beams at every step;
+ * Section 4.1.1: with the cache split, only the per-beam part Cache_K_t /
+ * Cache_V_t is reordered, the shared prefix and the encoder cache never are).
+ *
+ * The new hypothesis j of source b continues the old hypothesis
+ * parent[b*k + j] of the same source.  In place, for every head h and
+ * position tau < t:
+ *     K[b*k + j, h, tau, :] = old K[b*k + parent[b*k + j], h, tau, :]
+ * and the same for V.  Positions tau >= t keep their bytes; a hypothesis whose
+ * parent is itself, or outside [0, k), keeps its rows (they are neither read
+ * nor written).  Byte copies: the result is exact for any dtype.
+ *
+ * Arguments (device pointers except the sizes):
+ *   K, V     [B*k, H, T, D] of dtype; V may be NULL (then only K moves)
+ *   parent   [B*k] int32, the old beam (within the source) each new beam
+ *            continues, e.g. the beams a selection step kept
+ *   T, t     capacity and used positions of the cache (0 <= t <= T)
+ *   dtype    FS_F32 or FS_BF16
+ *   stream   hipStream_t (NULL = default stream)
+ * Supported: 1 <= k <= 16 and D*esize a multiple of 4 bytes.  16-byte moves
+ * when the pointers are 16-byte aligned and T*D*esize and t*D*esize are
+ * multiples of 16; 4-byte moves otherwise.
+ * Errors: FS_ERR_INVALID_ARG for negative sizes, t > T, null K or parent,
+ * pointers not 4-byte aligned, K overlapping V, or parent overlapping the
+ * cache; FS_ERR_UNSUPPORTED for k, dtype or D outside the set above or a
+ * cache too large for one launch; FS_ERR_HIP for a failed launch.  B, H, D
+ * or t == 0 returns FS_OK with no launch.
+ */
+int fs_cache_reorder(void *K, void *V, const int32_t *parent, int B, int k, int H, int T, int t, int D, int dtype,
+                     void *stream);
 
 #ifdef __cplusplus
 }

@@ -37,6 +37,7 @@ SIGNATURES = [
     ("fs_beam_select_workspace_bytes", _c_size, [_c_int] * 4),
     ("fs_beam_select", _c_int,
      [_vp, _vp, _vp, _c_int, _c_int, _c_int, _vp, _vp, _vp] + [_c_int] * 4 + [_vp, _c_size, _vp]),
+    ("fs_cache_reorder", _c_int, [_vp, _vp, _vp] + [_c_int] * 7 + [_vp]),
 ]
 
 _lib = None

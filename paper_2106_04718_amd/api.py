@@ -267,3 +267,34 @@ def beam_select(logits: torch.Tensor, beam_scores: torch.Tensor, k: int, c: int,
             out[1].data_ptr(), out[2].data_ptr(), B, int(k), V, int(c), workspace.data_ptr(),
             workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
     return out
+
+
+def cache_reorder(K: torch.Tensor, V: torch.Tensor | None, parent: torch.Tensor, k: int,
+                  t: int | None = None) -> None:
+    """Per-beam cache reorder after a selection step (Section 2.2 cache
+    maintenance; Section 4.1.1), in place.
+
+    K, V [B*k, H, T, D] float32 or bfloat16 (V may be None); parent [B*k]
+    int32, the old beam (within its source) each new hypothesis continues.
+    Rows tau < ``t`` (default T) of hypothesis b*k + j become those of
+    b*k + parent[b*k + j]; other rows, and beams whose parent is themselves or
+    outside [0, k), keep their bytes.
+    """
+    _need_cuda("K", K)
+    _need_cuda("parent", parent)
+    if K.dim() != 4 or K.dtype not in _DTYPES or not K.is_contiguous():
+        raise ValueError("K must be a contiguous float32/bfloat16 [B*k, H, T, D] tensor")
+    rows, H, T, D = K.shape
+    if k < 1 or rows % k:
+        raise ValueError(f"rows={rows} is not a multiple of k={k}")
+    dev = K.device
+    if V is not None:
+        _need_cuda("V", V)
+        if V.shape != K.shape or V.dtype != K.dtype or V.device != dev or not V.is_contiguous():
+            raise ValueError("V must match K (shape, dtype, device, contiguous)")
+    if parent.dtype != torch.int32 or parent.shape != (rows,) or parent.device != dev:
+        raise ValueError("parent must be int32 [B*k] on K's device")
+    tp = T if t is None else int(t)
+    with _on(dev):
+        _N.check(_N.ext().fs_cache_reorder(K.data_ptr(), 0 if V is None else V.data_ptr(), parent.data_ptr(),
+                                           rows // k, int(k), H, T, tp, D, _DTYPES[K.dtype], _stream_ptr(dev)))

@@ -335,4 +335,35 @@ int fs_beam_select(const float *logits, const float *beam_scores, const int32_t 
     return FS_OK;
 }
 
+
+int fs_cache_reorder(void *K, void *V, const int32_t *parent, int B, int k, int H, int T, int t, int D, int dtype,
+                     void *stream)
+{
+    g_last_error.clear();
+    if (B < 0 || k < 0 || H < 0 || T < 0 || t < 0 || D < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (B=%d k=%d H=%d T=%d t=%d D=%d)", B, k, H, T, t, D);
+    if (t > T) return fail(FS_ERR_INVALID_ARG, "t=%d > T=%d", t, T);
+    if (dtype != FS_F32 && dtype != FS_BF16)
+        return fail(FS_ERR_UNSUPPORTED, "dtype %d is not FS_F32 or FS_BF16", dtype);
+    if (k < 1 || k > 16) return fail(FS_ERR_UNSUPPORTED, "beam size k=%d outside [1, 16]", k);
+    const int esize = dtype == FS_BF16 ? 2 : 4;
+    if (((long long)D * esize) % 4 != 0)
+        return fail(FS_ERR_UNSUPPORTED, "a row of D=%d elements is not a whole number of 4-byte words", D);
+    if (B == 0 || H == 0 || t == 0 || D == 0) return FS_OK;  // nothing moves
+    if (!K || !parent) return fail(FS_ERR_INVALID_ARG, "null pointer (K=%p parent=%p)", K, (const void *)parent);
+    if (!aligned(K, 4) || !aligned(V, 4) || !aligned(parent, 4))
+        return fail(FS_ERR_INVALID_ARG, "K, V and parent must be 4-byte aligned");
+    const long long beam_bytes = (long long)H * T * D * esize;
+    if ((long long)k * beam_bytes > INT_MAX || (long long)t * D * esize > INT_MAX ||
+        (long long)2 * B * H * (((long long)t * D * esize / 4 + 255) / 256) > UINT_MAX)
+        return fail(FS_ERR_UNSUPPORTED, "cache too large for one launch (B=%d k=%d H=%d T=%d D=%d)", B, k, H, T, D);
+    const size_t cache_bytes = (size_t)B * k * beam_bytes;
+    if (overlaps(K, cache_bytes, V, V ? cache_bytes : 0)) return fail(FS_ERR_INVALID_ARG, "K overlaps V");
+    if (overlaps(K, cache_bytes, parent, (size_t)B * k * 4) || overlaps(V, V ? cache_bytes : 0, parent, (size_t)B * k * 4))
+        return fail(FS_ERR_INVALID_ARG, "parent overlaps the cache");
+    hipError_t e = fs::launch_cache_reorder(K, V, parent, B, k, H, T, t, D, esize, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "fs_cache_reorder launch");
+    return FS_OK;
+}
+
 }  // extern "C"

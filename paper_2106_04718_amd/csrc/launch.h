@@ -61,4 +61,10 @@ hipError_t launch_beam_select(const float *logits, const float *beam_scores, con
                               int k, int V, int c, unsigned long long *workspace, unsigned long long epoch,
                               hipStream_t stream);
 
+// Per-beam cache reorder: the chunk size (16 or 4 bytes) the kernel uses for
+// these pointers and sizes, and the launch (K and, if not null, V).
+int cache_reorder_chunk(const void *K, const void *V, int T, int t, int D, int esize);
+hipError_t launch_cache_reorder(void *K, void *V, const int32_t *parent, int B, int k, int H, int T, int t, int D,
+                                int esize, hipStream_t stream);
+
 }  // namespace fs

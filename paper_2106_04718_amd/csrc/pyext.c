@@ -86,6 +86,16 @@ static PyObject *py_beam_select(PyObject *self, PyObject *const *args, Py_ssize_
     return PyLong_FromLong(st);
 }
 
+static PyObject *py_cache_reorder(PyObject *self, PyObject *const *args, Py_ssize_t nargs) {
+    unsigned long long u[11];
+    int v[11];
+    (void)self;
+    if (unpack(args, nargs, "pppiiiiiiip", u, v)) return NULL;
+    int st = fs_cache_reorder(PTR(0), PTR(1), (const int32_t *)PTR(2), v[3], v[4], v[5], v[6], v[7], v[8], v[9],
+                              PTR(10));
+    return PyLong_FromLong(st);
+}
+
 static PyObject *py_last_error(PyObject *self, PyObject *unused) {
     (void)self;
     (void)unused;
@@ -103,6 +113,8 @@ static PyMethodDef methods[] = {
     {"fs_beam_select", (PyCFunction)(void (*)(void))py_beam_select, METH_FASTCALL,
      "fs_beam_select(logits, beam_scores, tokens, ld_tokens, t, n, out_scores, out_beam, out_token, B, k, V, c, "
      "workspace, workspace_bytes, stream)"},
+    {"fs_cache_reorder", (PyCFunction)(void (*)(void))py_cache_reorder, METH_FASTCALL,
+     "fs_cache_reorder(K, V, parent, B, k, H, T, t, D, dtype, stream)"},
     {"fs_last_error", py_last_error, METH_NOARGS, "fs_last_error() -> str"},
     {NULL, NULL, 0, NULL},
 };

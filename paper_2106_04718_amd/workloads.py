@@ -290,3 +290,20 @@ def select_inputs(cfg, planted: int = 1) -> dict:
     bs = -np.sort(-bs, axis=1)
     return {"logits": d["logits"], "tokens": tokens, "beam_scores": bs.astype(np.float32).reshape(-1),
             "n": cfg.n, "t": cfg.t, "k": cfg.k, "c": 2 * cfg.k, "B": cfg.B, "V": cfg.V}
+
+
+def reorder_inputs(cfg) -> dict:
+    """Parents of one per-beam cache reorder on a decode-step config.
+
+    The new hypothesis j of source b continues old beam parent[b*k + j]:
+    floor(k * u^2) with u ~ U[0, 1), which favours the best beams as beam
+    search does, from SeedSequence([210604718, cfg, 2000]).  The cache is one
+    decoder layer's self-attention K and V, [B*k, H, T, D] with T = t = the
+    config's history length (the last step of generation); its contents do
+    not matter to a byte copy.
+    """
+    cfg = get(cfg)
+    rng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, cfg.index, 2000]))
+    parent = np.floor(cfg.k * rng.random(cfg.B * cfg.k) ** 2).astype(np.int32)
+    return {"parent": parent, "B": cfg.B, "k": cfg.k, "H": cfg.H, "T": cfg.t, "t": cfg.t, "D": cfg.D,
+            "dtype": cfg.dtype}

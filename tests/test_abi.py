@@ -160,3 +160,72 @@ def test_marshalling_module_reaches_the_same_library():
         E.fs_ngram_block(FAKE, 4, 2)
     with pytest.raises(OverflowError):
         E.fs_ngram_block(FAKE, 1 << 40, 2, 5, 3, FAKE * 2, 7, None)
+
+
+def select(**kw):
+    a = dict(logits=FAKE, bs=FAKE * 64, tokens=FAKE * 128, ld=8, t=8, n=3, os=FAKE * 256, ob=FAKE * 320,
+             ot=FAKE * 384, B=2, k=4, V=100, c=8, ws=FAKE * 512, wsb=1 << 20, stream=None)
+    a.update(kw)
+    return N.lib().fs_beam_select(a["logits"], a["bs"], a["tokens"], a["ld"], a["t"], a["n"], a["os"], a["ob"],
+                                  a["ot"], a["B"], a["k"], a["V"], a["c"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(c=17), N.FS_ERR_UNSUPPORTED, "c=17"),
+    (dict(c=0), N.FS_ERR_UNSUPPORTED, "c=0"),
+    (dict(k=17), N.FS_ERR_UNSUPPORTED, "k=17"),
+    (dict(k=1, V=3, c=4), N.FS_ERR_INVALID_ARG, "c=4 > k*V"),
+    (dict(B=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(n=-1), N.FS_ERR_INVALID_ARG, "n=-1"),
+    (dict(ld=4), N.FS_ERR_INVALID_ARG, "ld_tokens"),
+    (dict(logits=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(os=FAKE * 256 + 2), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(wsb=8), N.FS_ERR_INVALID_ARG, "workspace"),
+    (dict(ob=FAKE * 256 + 4), N.FS_ERR_INVALID_ARG, "overlap"),
+])
+def test_select_rejects(kw, status, needle):
+    assert select(**kw) == status
+    assert needle in N.last_error()
+
+
+def test_select_workspace_bytes_and_empty_batch():
+    f = N.lib().fs_beam_select_workspace_bytes
+    assert f(0, 4, 100, 8) == 0
+    assert f(2, 4, 100, 8) == 2 * 4 * 1 * (2 + 2 * 8) * 8      # one slice per row at V = 100
+    assert f(2, 17, 100, 8) == ctypes.c_size_t(-1).value
+    assert select(B=0, logits=None, bs=None, tokens=None, os=None, ob=None, ot=None, ws=None, wsb=0) == N.FS_OK
+
+
+def reorder(**kw):
+    a = dict(K=FAKE, V=FAKE * 64, parent=FAKE * 128, B=2, k=4, H=2, T=10, t=5, D=16, dtype=N.FS_BF16, stream=None)
+    a.update(kw)
+    return N.lib().fs_cache_reorder(a["K"], a["V"], a["parent"], a["B"], a["k"], a["H"], a["T"], a["t"], a["D"],
+                                    a["dtype"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(t=11), N.FS_ERR_INVALID_ARG, "t=11 > T=10"),
+    (dict(B=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(k=17), N.FS_ERR_UNSUPPORTED, "k=17"),
+    (dict(k=0), N.FS_ERR_UNSUPPORTED, "k=0"),
+    (dict(dtype=7), N.FS_ERR_UNSUPPORTED, "dtype"),
+    (dict(D=3), N.FS_ERR_UNSUPPORTED, "4-byte"),
+    (dict(K=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(parent=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(V=FAKE * 64 + 2), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(V=FAKE + 64), N.FS_ERR_INVALID_ARG, "K overlaps V"),
+    (dict(parent=FAKE + 64), N.FS_ERR_INVALID_ARG, "parent overlaps"),
+])
+def test_reorder_rejects(kw, status, needle):
+    assert reorder(**kw) == status
+    assert needle in N.last_error()
+
+
+def test_reorder_nothing_to_move_returns_ok_without_launch():
+    assert reorder(K=None, parent=None, t=0) == N.FS_OK
+    assert reorder(K=None, parent=None, B=0) == N.FS_OK
+    assert reorder(K=None, parent=None, H=0) == N.FS_OK
+    # the marshalling module reaches the same entry point
+    E = N.ext()
+    assert E.fs_cache_reorder(FAKE, FAKE, FAKE * 128, 2, 4, 2, 10, 5, 16, N.FS_BF16, None) == N.FS_ERR_INVALID_ARG
+    assert "K overlaps V" in E.fs_last_error()
