@@ -163,8 +163,8 @@ def copy_calibrate(gib: float) -> None:
 def main() -> int:
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the decode step shards by source with no exchange; see DESIGN.md)",
+        print(f"bench.py: the benchmark runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the decode step would shard by source with no exchange between GPUs)",
               file=sys.stderr)
         return 2
     import numpy as np

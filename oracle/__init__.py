@@ -19,6 +19,9 @@ module only marshals numpy arrays into it:
 * :func:`cache_reorder` -- the per-beam cache reorder after a selection step
   (Section 2.2 cache maintenance, Section 4.1.1): each new hypothesis takes
   its parent's generated-token cache.
+* :func:`ancestry_step` and :func:`prefix_attn_indirect` -- the same
+  maintenance without moving rows: a table of which beam's row holds each
+  generated token, and the split-cache attention read through it.
 
 bf16 inputs are passed as their uint16 bit patterns and widened exactly to
 fp64 here (a bf16 value is the upper half of an fp32 value), so the oracle
@@ -56,6 +59,8 @@ def _lib():
         lib.oracle_beam_select.restype = ctypes.c_int
         lib.oracle_cache_reorder.argtypes = [ctypes.c_void_p, _ip] + [ctypes.c_int] * 7
         lib.oracle_cache_reorder.restype = ctypes.c_int
+        lib.oracle_ancestry_step.argtypes = [_ip, ctypes.c_int, _ip] + [ctypes.c_int] * 3
+        lib.oracle_ancestry_step.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         lib.oracle_num_threads.restype = ctypes.c_int
         lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
@@ -234,3 +239,45 @@ def cache_reorder(cache, parent, k: int, t: int) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle_cache_reorder rejected its arguments")
     return x
+
+
+def ancestry_step(anc, parent, k: int, t: int) -> np.ndarray:
+    """One step of the ancestry table (see ``oracle_ancestry_step``).
+
+    anc [B*k, ld] int32 with ld > t; parent [B*k] int32.  Returns the updated
+    copy: columns tau < t of hypothesis b*k + j become those of
+    b*k + parent[b*k + j], column t becomes j, later columns are kept.
+    """
+    a = np.array(anc, dtype=np.int32, copy=True, order="C")
+    par = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    if a.ndim != 2 or k < 1 or a.shape[0] % k or par.shape != (a.shape[0],):
+        raise ValueError("anc must be [B*k, ld] and parent [B*k]")
+    rc = _lib().oracle_ancestry_step(a.ctypes.data_as(_ip), a.shape[1], par.ctypes.data_as(_ip),
+                                     a.shape[0] // k, int(k), int(t))
+    if rc != 0:
+        raise ValueError("oracle_ancestry_step rejected its arguments")
+    return a
+
+
+def gather_generated(Kt, anc, k: int, t: int) -> np.ndarray:
+    """The generated-token cache as hypothesis r sees it through the table:
+    out[r, h, tau] = Kt[b*k + anc[r, tau], h, tau] for tau < t (entries
+    outside [0, k) read r's own row); positions tau >= t are copied as they
+    are."""
+    Kt = np.asarray(Kt)
+    anc = np.asarray(anc)
+    rows = Kt.shape[0]
+    out = Kt.copy()
+    own = np.arange(rows) % k
+    for tau in range(t):
+        a = anc[:, tau]
+        a = np.where((a >= 0) & (a < k), a, own)
+        out[:, :, tau] = Kt[(np.arange(rows) // k) * k + a, :, tau]
+    return out
+
+
+def prefix_attn_indirect(q, Kp, Vp, prefix_len, Kt, Vt, anc, t: int) -> np.ndarray:
+    """Split-cache self-attention whose generated rows are read through the
+    ancestry table (definition: gather the rows, then :func:`prefix_attn`)."""
+    k = np.asarray(q).shape[1]
+    return prefix_attn(q, Kp, Vp, prefix_len, gather_generated(Kt, anc, k, t), gather_generated(Vt, anc, k, t), t)

@@ -22,6 +22,8 @@
  *                       log-probabilities with the n-gram bans applied.
  *   oracle_cache_reorder the per-beam cache reorder that follows a selection
  *                       step (Section 2.2, cache maintenance; Section 4.1.1).
+ *   oracle_ancestry_step the reorder-free form of that maintenance: a table of
+ *                       which beam's cache row holds each generated token.
  */
 #include <math.h>
 #include <stddef.h>
@@ -442,6 +444,58 @@ int oracle_cache_reorder(unsigned char *cache, const int32_t *parent, int B, int
                 for (int tau = 0; tau < t; ++tau)
                     memcpy(src + (size_t)j * beam + ((size_t)h * T + tau) * row,
                            old + (size_t)from * beam + ((size_t)h * T + tau) * row, row);
+        }
+        free(old);
+    }
+    return bad;
+}
+
+/*
+ * Ancestry table of the generated-token cache: the same cache maintenance as
+ * oracle_cache_reorder (Section 2.2; Section 4.1.1) without moving the rows.
+ *
+ * Each hypothesis writes the K/V of its tau-th generated token to its own
+ * cache row, at position tau, and never moves it.  anc[r, tau] (tau <= the
+ * step) is the beam, within r's source, whose row holds the tau-th token of
+ * hypothesis r.  After a selection step at which each hypothesis holds t
+ * tokens and the new hypothesis j of source b continues old beam
+ * parent[b*k + j]:
+ *     anc[b*k + j, tau] = old anc[b*k + parent[b*k + j], tau]   for tau < t
+ *     anc[b*k + j, t]   = j          (the step's new token, in j's own row)
+ * A parent outside [0, k) keeps the hypothesis' own history (as in
+ * oracle_cache_reorder).  Reading row anc[r, tau] of r's source at position
+ * tau then gives exactly what the physically reordered cache holds at
+ * (r, tau).
+ *
+ * anc is [B*k, ld] int32 (ld > t), updated in place from a copy of each
+ * source's old rows.  Returns 0, or 1 for invalid arguments.
+ */
+int oracle_ancestry_step(int32_t *anc, int ld, const int32_t *parent, int B, int k, int t)
+{
+    if (B < 0 || k < 1 || t < 0 || ld <= t)
+        return 1;
+    if (B == 0)
+        return 0;
+    if (!anc || !parent)
+        return 1;
+    int bad = 0;
+
+#pragma omp parallel for schedule(static)
+    for (int b = 0; b < B; ++b) {
+        int32_t *src = anc + (size_t)b * k * ld;
+        int32_t *old = malloc((size_t)k * ld * sizeof(int32_t));
+        if (!old) {
+#pragma omp atomic write
+            bad = 1;
+            continue;
+        }
+        memcpy(old, src, (size_t)k * ld * sizeof(int32_t));
+        for (int j = 0; j < k; ++j) {
+            const int32_t pj = parent[(size_t)b * k + j];
+            const int from = (pj >= 0 && pj < k) ? pj : j;
+            for (int tau = 0; tau < t; ++tau)
+                src[(size_t)j * ld + tau] = old[(size_t)from * ld + tau];
+            src[(size_t)j * ld + t] = j;
         }
         free(old);
     }
