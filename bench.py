@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--config", default="bart",
                     help="decode step: tiny | bart | t5 | prophetnet | large; "
                          "split-cache self-attention step: gpt2 | tiny_prefix")
-    ap.add_argument("--part", default="step", choices=("step", "select", "reorder"),
+    ap.add_argument("--part", default="step", choices=("step", "select", "reorder", "indirect"),
                     help="step: the decode step (cross-attention + n-gram blocking); "
                          "select: the beam-selection step on the same config's logits")
     ap.add_argument("--rounds", type=int, default=5,
@@ -179,7 +179,12 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     if args.config in workloads.PREFIX_CONFIGS:
+        if args.part == "indirect":
+            return bench_indirect(args, workloads.PREFIX_CONFIGS[args.config], dev)
         return bench_prefix(args, workloads.PREFIX_CONFIGS[args.config], dev)
+    if args.part == "indirect":
+        print("bench.py: --part indirect runs on a split-cache config (gpt2, tiny_prefix)", file=sys.stderr)
+        return 2
     if args.part == "select":
         return bench_select(args, workloads.get(args.config), dev)
     if args.part == "reorder":
@@ -407,6 +412,144 @@ def bench_prefix(args, cfg, dev) -> int:
         while True:
             c0 = time.perf_counter()
             ref = oracle.prefix_attn(qd, Kpd, Vpd, lens, Ktd, Vtd, t)
+            times.append(time.perf_counter() - c0)
+            if (args.cpu_reps and len(times) >= args.cpu_reps) or \
+                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                break
+        sec = float(np.median(times))
+        err = float(np.max(np.abs(out0 - ref)))
+        tol = 2e-2 if cfg.dtype == "bf16" else 1e-5 * float(np.max(np.abs(ref)))
+        log(f"oracle: {sec * 1e3:.1f} ms per step on {oracle.num_threads()} threads; attn max abs err {err:.3e}")
+        line["cpu_baseline"] = {"value": round(b / sec / 1e9, 4), "unit": "GB/s", "cores": oracle.num_threads(),
+                                "kind": "oracle",
+                                "sample": f"whole {cfg.name}-shaped step, K/V set 0, median of {len(times)} reps, "
+                                          f"{sec * 1e3:.1f} ms per step"}
+        line["parity"] = {"attn_max_abs_err": err, "attn_tol": tol, "attn_ok": err <= tol}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def bench_indirect(args, cfg, dev) -> int:
+    """Split-cache self-attention with the generated rows read through an
+    ancestry table (the reorder-free cache maintenance).  A step is one
+    fs_beam_prefix_attn_indirect call; the same run times the direct call on
+    the same inputs, the fs_cache_reorder of that layer's generated K/V that
+    the table replaces, and one fs_beam_ancestry_step (once per decode step,
+    shared by the layers)."""
+    import numpy as np
+    import torch
+
+    from paper_2106_04718_amd import api, workloads
+
+    def dev_tensor(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    t0 = time.perf_counter()
+    base = workloads.prefix_inputs(cfg)
+    am = workloads.ancestry_inputs(cfg)
+    lens, t = base["prefix_len"], base["t"]
+    set_bytes = sum(base[x].nbytes for x in ("Kp", "Vp", "Kt", "Vt"))
+    R = max(1, math.ceil(args.rotate_gib * (1 << 30) / set_bytes))
+    q, lens_d = dev_tensor(base["q"]), dev_tensor(lens)
+    anc_d, par_d = dev_tensor(am["anc"]), dev_tensor(am["parent"])
+    anc_scratch = anc_d.clone()
+    sets = [tuple(dev_tensor(base[x]) for x in ("Kp", "Vp", "Kt", "Vt"))]
+    for r in range(1, R):
+        d = workloads.prefix_inputs(cfg, rep=r)
+        sets.append(tuple(dev_tensor(d[x]) for x in ("Kp", "Vp", "Kt", "Vt")))
+        del d
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_prefix_attn_workspace_bytes(cfg.B, cfg.k, cfg.H, cfg.N, cfg.T, cfg.D, tdt),
+                           dev)
+    torch.cuda.synchronize()
+    log(f"config={cfg.name} indirect: K/V sets={R} ({R * set_bytes / 2**30:.2f} GiB) inputs ready in "
+        f"{time.perf_counter() - t0:.1f}s")
+    stream = torch.cuda.current_stream(dev)
+
+    def timed(fn, K):
+        for i in range(args.warmup):
+            fn(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(K):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / K
+
+    def step(i: int):
+        Kp, Vp, Kt, Vt = sets[i % R]
+        api.beam_prefix_attn(q, Kp, Vp, lens_d, Kt, Vt, t, out=out, workspace=ws, anc=anc_d)
+
+    def direct(i: int):
+        Kp, Vp, Kt, Vt = sets[i % R]
+        api.beam_prefix_attn(q, Kp, Vp, lens_d, Kt, Vt, t, out=out, workspace=ws)
+
+    def reorder(i: int):
+        _, _, Kt, Vt = sets[i % R]
+        api.cache_reorder(Kt, Vt, par_d, cfg.k, t)
+
+    def anc_step(i: int):
+        api.ancestry_step(anc_scratch, par_d, cfg.k, min(t, cfg.T - 1))
+
+    step(0)
+    torch.cuda.synchronize()
+    out0 = out.float().cpu().numpy().astype(np.float64)
+    K_ = args.steps
+    step_us = timed(step, K_)
+    spread = launch_spread(stream, step, K_)
+    direct_us = timed(direct, K_)
+    reorder_us = timed(reorder, K_)
+    anc_us = timed(anc_step, K_)
+    b = prefix_bytes(cfg, lens, t) + cfg.B * cfg.k * t * 4
+    gbps = b / (step_us * 1e-6) / 1e9
+    copy_gbps = copy_bandwidth(dev)
+    log(f"indirect step {step_us:.2f} us = {gbps:.0f} GB/s ({100 * gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s); direct "
+        f"{direct_us:.2f} us; the layer's reorder it replaces {reorder_us:.2f} us; ancestry step {anc_us:.2f} us "
+        f"per decode step")
+    line = {
+        "metric": "split-cache self-attention step through an ancestry table, µs and achieved HBM GB/s, GPT2 shape",
+        "value": round(gbps, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K_,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_us * 1e-3, 6),
+        "step_us": round(step_us, 3),
+        "step_us_spread": spread,
+        "direct_step_us": round(direct_us, 3),
+        "reorder_us": round(reorder_us, 3),
+        "ancestry_step_us": round(anc_us, 3),
+        "per_layer_saving_us": round(direct_us + reorder_us - step_us, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded; shared prefix K/V per sample, per-beam generated K/V, ancestry floor(k*u^2))",
+        "config": {"workload": (f"{cfg.name}-shaped split-cache self-attention step through an ancestry table: "
+                                f"B={cfg.B} k={cfg.k} H={cfg.H} D={cfg.D}, shared prefix N={cfg.N}, {t} generated "
+                                f"tokens per beam (capacity {cfg.T}), {cfg.dtype}"),
+                   "B": cfg.B, "k": cfg.k, "H": cfg.H, "D": cfg.D, "N": cfg.N, "T": cfg.T, "t": t,
+                   "kv_sets_rotated": R, "bytes_per_step": b},
+        "copy_gbps": round(copy_gbps, 1),
+        "roofline": {"bound": "hbm", "kernel": "fs_beam_prefix_attn_indirect", "achieved": round(gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "algorithmic_bytes_per_launch": b,
+                     "traffic": load_traffic(args.traffic, cfg.name + "-indirect")},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        times, ref = [], None
+        while True:
+            c0 = time.perf_counter()
+            ref = oracle.prefix_attn_indirect(base["q"], base["Kp"], base["Vp"], lens, base["Kt"], base["Vt"],
+                                              am["anc"], t)
             times.append(time.perf_counter() - c0)
             if (args.cpu_reps and len(times) >= args.cpu_reps) or \
                     (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):

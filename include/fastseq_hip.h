@@ -19,6 +19,10 @@
  *   fs_cache_reorder    the per-beam cache reorder after a selection step
  *                       (Section 2.2, cache maintenance; Section 4.1.1), in
  *                       place.
+ *   fs_beam_ancestry_step, fs_beam_prefix_attn_indirect
+ *                       the same maintenance without moving rows: an ancestry
+ *                       table of the generated tokens, and the split-cache
+ *                       attention that reads its generated rows through it.
  *
  * Conventions shared by every entry point
  *   - Pointers named "device" are HIP device memory; the caller owns every
@@ -284,6 +288,50 @@ int fs_beam_select(const float *logits, const float *beam_scores, const int32_t 
  */
 int fs_cache_reorder(void *K, void *V, const int32_t *parent, int B, int k, int H, int T, int t, int D, int dtype,
                      void *stream);
+
+/*
+ * Ancestry table of the generated-token cache: the per-beam maintenance of
+ * fs_cache_reorder (Section 2.2; Section 4.1.1) without moving any row.
+ * Each hypothesis writes the K/V of its tau-th generated token to its own
+ * row at position tau and never moves it; anc[r, tau] is the beam, within
+ * r's source, whose row holds the tau-th token of hypothesis r.  After a
+ * selection step at which every hypothesis holds t tokens, and before the
+ * step's new token is written:
+ *     anc[b*k + j, tau] = old anc[b*k + parent[b*k + j], tau]   tau < t
+ *     anc[b*k + j, t]   = j
+ * in place.  Columns past t keep their values; a parent outside [0, k)
+ * keeps the hypothesis' own history.  Start from any table with t = 0.
+ *
+ * Arguments (device pointers except the sizes):
+ *   anc      [B*k, ld_anc] int32, updated in place (t < ld_anc)
+ *   parent   [B*k] int32, the old beam each new hypothesis continues
+ *   stream   hipStream_t (NULL = default stream)
+ * Supported: 1 <= k <= 16.
+ * Errors: FS_ERR_INVALID_ARG for negative sizes, t >= ld_anc, null or
+ * misaligned pointers, or parent overlapping anc; FS_ERR_UNSUPPORTED for k
+ * or a table too large; FS_ERR_HIP for a failed launch.  B == 0 returns
+ * FS_OK with no launch.
+ */
+int fs_beam_ancestry_step(int32_t *anc, int ld_anc, const int32_t *parent, int B, int k, int t, void *stream);
+
+/*
+ * fs_beam_prefix_attn with the generated rows read through an ancestry
+ * table (fs_beam_ancestry_step): for hypothesis r = b*k + i, generated row
+ * tau (tau < t) is row tau of the block of hypothesis b*k + anc[r, tau] of
+ * Kt/Vt; an entry outside [0, k) reads r's own block.  Everything else --
+ * arguments, layouts, the prefix part, errors -- is that of
+ * fs_beam_prefix_attn; with anc[r, tau] = i for all tau it returns the same
+ * bits.  The rows of one source's k beams are read through one buffer
+ * range, so k*H*T*D*esize must stay below 2 GiB.
+ *   anc      [B*k, ld_anc] int32 (ld_anc >= t); not read when t == 0
+ * Additional errors: FS_ERR_INVALID_ARG for a null or misaligned anc with
+ * t > 0, ld_anc < t, or out overlapping anc; FS_ERR_UNSUPPORTED for the
+ * 2 GiB limit.
+ */
+int fs_beam_prefix_attn_indirect(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                                 const void *Kt, const void *Vt, const int32_t *anc, int ld_anc, int T, int t,
+                                 void *out, int B, int k, int H, int N, int D, int dtype, void *workspace,
+                                 size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -38,6 +38,9 @@ SIGNATURES = [
     ("fs_beam_select", _c_int,
      [_vp, _vp, _vp, _c_int, _c_int, _c_int, _vp, _vp, _vp] + [_c_int] * 4 + [_vp, _c_size, _vp]),
     ("fs_cache_reorder", _c_int, [_vp, _vp, _vp] + [_c_int] * 7 + [_vp]),
+    ("fs_beam_ancestry_step", _c_int, [_vp, _c_int, _vp] + [_c_int] * 3 + [_vp]),
+    ("fs_beam_prefix_attn_indirect", _c_int,
+     [_vp] * 7 + [_c_int] * 3 + [_vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
 ]
 
 _lib = None

@@ -130,12 +130,15 @@ def beam_prefix_attn_workspace_bytes(B: int, k: int, H: int, N: int, T: int, D: 
 
 def beam_prefix_attn(q: torch.Tensor, Kp: torch.Tensor, Vp: torch.Tensor, prefix_len: torch.Tensor,
                      Kt: torch.Tensor, Vt: torch.Tensor, t: int, out: torch.Tensor | None = None,
-                     workspace: torch.Tensor | None = None) -> torch.Tensor:
+                     workspace: torch.Tensor | None = None, anc: torch.Tensor | None = None) -> torch.Tensor:
     """Self-attention over a split cache (Appendix A, Eq. 2-3).
 
     q [B,k,H,D]; Kp, Vp [B,H,N,D] shared prefix with prefix_len [B] int32;
     Kt, Vt [B*k,H,T,D] per-beam generated tokens of which rows [0, t) are
-    used.  One softmax covers both parts.  Returns out [B,k,H,D].
+    used.  One softmax covers both parts.  Returns out [B,k,H,D].  With
+    ``anc`` ([B*k, ld] int32 ancestry table, see :func:`ancestry_step`) the
+    generated row tau of hypothesis b*k + i is read from the block of
+    hypothesis b*k + anc[b*k + i, tau] instead of its own.
     """
     for name, x in (("q", q), ("Kp", Kp), ("Vp", Vp), ("prefix_len", prefix_len), ("Kt", Kt), ("Vt", Vt)):
         _need_cuda(name, x)
@@ -162,12 +165,50 @@ def beam_prefix_attn(q: torch.Tensor, Kp: torch.Tensor, Vp: torch.Tensor, prefix
         workspace = new_workspace(beam_prefix_attn_workspace_bytes(B, k, H, Np, T, D, q.dtype), dev)
     else:
         _need_cuda("workspace", workspace)
+    if anc is not None:
+        _need_cuda("anc", anc)
+        if anc.dtype != torch.int32 or anc.dim() != 2 or anc.shape[0] != B * k or anc.device != dev:
+            raise ValueError("anc must be int32 [B*k, ld] on q's device")
+        if B * k > 1 and anc.shape[1] > 1 and anc.stride(1) != 1:
+            raise ValueError("anc must have unit column stride")
+        ld = anc.stride(0) if B * k > 1 else anc.shape[1]
+        with _on(dev):
+            _N.check(_N.ext().fs_beam_prefix_attn_indirect(
+                q.data_ptr(), Kp.data_ptr(), Vp.data_ptr(), prefix_len.data_ptr(), Kt.data_ptr(), Vt.data_ptr(),
+                anc.data_ptr(), ld, T, int(t), out.data_ptr(), B, k, H, Np, D, _DTYPES[q.dtype],
+                workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
+        return out
     with _on(dev):
         _N.check(_N.ext().fs_beam_prefix_attn(
             q.data_ptr(), Kp.data_ptr(), Vp.data_ptr(), prefix_len.data_ptr(), Kt.data_ptr(), Vt.data_ptr(),
             T, int(t), out.data_ptr(), B, k, H, Np, D, _DTYPES[q.dtype], workspace.data_ptr(),
             workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
     return out
+
+
+def ancestry_step(anc: torch.Tensor, parent: torch.Tensor, k: int, t: int) -> torch.Tensor:
+    """One step of the ancestry table, in place (the reorder-free cache
+    maintenance after a selection step).
+
+    anc [B*k, ld] int32 (ld > t); parent [B*k] int32, the old beam each new
+    hypothesis continues.  Columns tau < t of hypothesis b*k + j become those
+    of b*k + parent[b*k + j]; column t becomes j (its new token, written to
+    its own row).  Returns anc.
+    """
+    _need_cuda("anc", anc)
+    _need_cuda("parent", parent)
+    if anc.dtype != torch.int32 or anc.dim() != 2 or k < 1 or anc.shape[0] % k:
+        raise ValueError("anc must be int32 [B*k, ld]")
+    rows = anc.shape[0]
+    if rows > 1 and anc.shape[1] > 1 and anc.stride(1) != 1:
+        raise ValueError("anc must have unit column stride")
+    if parent.dtype != torch.int32 or parent.shape != (rows,) or parent.device != anc.device:
+        raise ValueError("parent must be int32 [B*k] on anc's device")
+    ld = anc.stride(0) if rows > 1 else anc.shape[1]
+    with _on(anc.device):
+        _N.check(_N.ext().fs_beam_ancestry_step(anc.data_ptr(), ld, parent.data_ptr(), rows // k, int(k), int(t),
+                                                _stream_ptr(anc.device)))
+    return anc
 
 
 def ngram_block(tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | None = None) -> torch.Tensor:

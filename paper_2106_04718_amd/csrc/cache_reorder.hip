@@ -133,7 +133,61 @@ hipError_t launch_chunks(unsigned char *K, unsigned char *V, const int32_t *pare
     return hipGetLastError();
 }
 
+// Ancestry step: block (source b, block of columns); lane tau owns column tau
+// of the source's k rows.  Columns tau < t take the parent's entry, column t
+// the beam's own index.  All loads come before all stores, so it is in place.
+template <int KMAX>
+__global__ __launch_bounds__(kThreads) void ancestry_step_kernel(int32_t *anc, int ld, const int32_t *parent, int k,
+                                                                 int t, int nblk)
+{
+    const int b = blockIdx.x / nblk;
+    const int tau = (blockIdx.x % nblk) * kThreads + (int)threadIdx.x;
+    if (tau > t) return;
+    int32_t *col = anc + (size_t)b * k * ld + tau;
+    // the column's entries first: they do not depend on the parents, so both
+    // sets of loads are in flight together
+    int32_t v[KMAX];
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) v[i] = (i < k && tau < t) ? col[(size_t)i * ld] : 0;
+    // the parents (wave-uniform), all loads issued before any is used
+    int par[KMAX];
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) par[j] = j < k ? parent[(size_t)b * k + j] : j;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) par[j] = (par[j] >= 0 && par[j] < k) ? par[j] : j;
+    if (tau < t) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): every load before the first store
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j) {
+            if (j < k && par[j] != j) {
+                int32_t x = v[0];
+#pragma unroll
+                for (int i = 1; i < KMAX; ++i) x = par[j] == i ? v[i] : x;
+                col[(size_t)j * ld] = x;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j)
+            if (j < k) col[(size_t)j * ld] = j;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_ancestry_step(int32_t *anc, int ld, const int32_t *parent, int B, int k, int t,
+                                hipStream_t stream)
+{
+    const int nblk = (t + 1 + kThreads - 1) / kThreads;
+    const dim3 gd((unsigned)((long long)B * nblk)), bd(kThreads);
+    if (k <= 4)
+        hipLaunchKernelGGL(ancestry_step_kernel<4>, gd, bd, 0, stream, anc, ld, parent, k, t, nblk);
+    else if (k <= 8)
+        hipLaunchKernelGGL(ancestry_step_kernel<8>, gd, bd, 0, stream, anc, ld, parent, k, t, nblk);
+    else
+        hipLaunchKernelGGL(ancestry_step_kernel<16>, gd, bd, 0, stream, anc, ld, parent, k, t, nblk);
+    return hipGetLastError();
+}
 
 int cache_reorder_chunk(const void *K, const void *V, int T, int t, int D, int esize) {
     // 16-byte chunks when every (hypothesis, head) block starts on a 16-byte

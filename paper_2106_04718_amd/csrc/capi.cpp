@@ -170,10 +170,15 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
     return FS_OK;
 }
 
-int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
-                        const void *Kt, const void *Vt, int T, int t, void *out,
-                        int B, int k, int H, int N, int D, int dtype,
-                        void *workspace, size_t workspace_bytes, void *stream)
+}  // extern "C"
+
+namespace {
+
+// Both split-cache entry points: without (anc == null) and with the
+// ancestry table of the generated rows.
+int prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len, const void *Kt,
+                const void *Vt, const int32_t *anc, int ld_anc, int T, int t, void *out, int B, int k, int H, int N,
+                int D, int dtype, void *workspace, size_t workspace_bytes, void *stream, bool indirect)
 {
     g_last_error.clear();
     if (T < 0 || t < 0) return fail(FS_ERR_INVALID_ARG, "negative size (T=%d t=%d)", T, t);
@@ -199,6 +204,17 @@ int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int
         return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
     if ((long long)B * k * H * ((long long)T * D) > (long long)INT_MAX * 16)
         return fail(FS_ERR_INVALID_ARG, "generated-token cache too large");
+    if (indirect && t > 0) {
+        if (!anc) return fail(FS_ERR_INVALID_ARG, "null ancestry table with t=%d > 0", t);
+        if (ld_anc < t) return fail(FS_ERR_INVALID_ARG, "ld_anc=%d < t=%d", ld_anc, t);
+        if (!aligned(anc, 4)) return fail(FS_ERR_INVALID_ARG, "anc must be 4-byte aligned");
+        // the rows of a source's k beams are read through one buffer range
+        if ((long long)k * H * T * D * (long long)esize > 0x7ff00000LL)
+            return fail(FS_ERR_UNSUPPORTED, "a source's generated-token cache exceeds 2 GiB (k=%d H=%d T=%d D=%d)",
+                        k, H, T, D);
+        if (overlaps(out, q_bytes, anc, ((size_t)(B * k - 1) * ld_anc + t) * 4))
+            return fail(FS_ERR_INVALID_ARG, "out overlaps the ancestry table");
+    }
     const size_t need = fs_beam_prefix_attn_workspace_bytes(B, k, H, N, T, D, dtype);
     if (workspace_bytes < need || (need > 0 && !workspace))
         return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed",
@@ -220,9 +236,52 @@ int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int
             if (lens[b] < 0 || lens[b] > N)
                 return fail(FS_ERR_INVALID_ARG, "prefix_len[%d] = %d outside [0, %d]", b, lens[b], N);
     }
-    hipError_t e = fs::launch_prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, T, t, out, B, k, H, N, D,
-                                          dtype == FS_BF16, static_cast<float *>(workspace), next_epoch(), s);
-    if (e != hipSuccess) return hip_fail(e, "fs_beam_prefix_attn launch");
+    hipError_t e = fs::launch_prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, T, t, indirect && t > 0 ? anc : nullptr,
+                                          ld_anc, out, B, k, H, N, D, dtype == FS_BF16,
+                                          static_cast<float *>(workspace), next_epoch(), s);
+    if (e != hipSuccess) return hip_fail(e, indirect ? "fs_beam_prefix_attn_indirect launch" : "fs_beam_prefix_attn launch");
+    return FS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                        const void *Kt, const void *Vt, int T, int t, void *out,
+                        int B, int k, int H, int N, int D, int dtype,
+                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    return prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, nullptr, 0, T, t, out, B, k, H, N, D, dtype, workspace,
+                       workspace_bytes, stream, false);
+}
+
+int fs_beam_prefix_attn_indirect(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
+                                 const void *Kt, const void *Vt, const int32_t *anc, int ld_anc, int T, int t,
+                                 void *out, int B, int k, int H, int N, int D, int dtype, void *workspace,
+                                 size_t workspace_bytes, void *stream)
+{
+    return prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, anc, ld_anc, T, t, out, B, k, H, N, D, dtype, workspace,
+                       workspace_bytes, stream, true);
+}
+
+int fs_beam_ancestry_step(int32_t *anc, int ld_anc, const int32_t *parent, int B, int k, int t, void *stream)
+{
+    g_last_error.clear();
+    if (B < 0 || k < 0 || t < 0 || ld_anc < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (B=%d k=%d t=%d ld_anc=%d)", B, k, t, ld_anc);
+    if (k < 1 || k > 16) return fail(FS_ERR_UNSUPPORTED, "beam size k=%d outside [1, 16]", k);
+    if (t >= ld_anc) return fail(FS_ERR_INVALID_ARG, "column t=%d does not exist (ld_anc=%d)", t, ld_anc);
+    if (B == 0) return FS_OK;
+    if (!anc || !parent) return fail(FS_ERR_INVALID_ARG, "null pointer (anc=%p parent=%p)", (void *)anc,
+                                     (const void *)parent);
+    if (!aligned(anc, 4) || !aligned(parent, 4)) return fail(FS_ERR_INVALID_ARG, "anc and parent must be 4-byte aligned");
+    if ((long long)B * k * ld_anc > (long long)INT_MAX * 4)
+        return fail(FS_ERR_UNSUPPORTED, "ancestry table too large (B=%d k=%d ld_anc=%d)", B, k, ld_anc);
+    if (overlaps(anc, (size_t)B * k * ld_anc * 4, parent, (size_t)B * k * 4))
+        return fail(FS_ERR_INVALID_ARG, "parent overlaps the ancestry table");
+    hipError_t e = fs::launch_ancestry_step(anc, ld_anc, parent, B, k, t, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "fs_beam_ancestry_step launch");
     return FS_OK;
 }
 

@@ -291,11 +291,34 @@ constexpr int kMaxSpins = 1 << 14;
 // stream (rows of kLpr 16-byte slices).  On return m[i], l[i] (base-2 max and
 // sum of exp2) are wave-uniform and acc[i][e] holds, in every lane, the
 // unnormalised output for dims sub*kEpl + e.  prow is this wave's LDS area.
-template <int D, bool BF16, int KB>
+// Rows of a generated-token tile read through an ancestry table: row j of
+// the hypothesis is row j of the block of beam row[j] of its source (an entry
+// outside [0, k) reads the hypothesis' own block, `self`).  The K/V pointers
+// then address the source's beam-0 block, and `stride` is the distance in
+// bytes between the blocks of two beams (H * T * row bytes).
+struct Anc {
+    const int32_t *row;
+    int self, k, stride;
+    // beams of this lane's rows of the first tile (t0 = 0), when `early`:
+    // loaded before the tile, so that its K/V loads need not wait for them
+    int first[kIt];
+    bool early;
+    __device__ __forceinline__ int beam(int j) const {
+        const int a = row[j];
+        return (a >= 0 && a < k) ? a : self;
+    }
+    // the beam of row j = t0 + u * rows-per-load + lane group, clamped to j1 - 1
+    __device__ __forceinline__ int beam_at(int t0, int u, int j) const {
+        return (early && t0 == 0) ? first[u] : beam(j);
+    }
+};
+
+template <int D, bool BF16, int KB, bool IND = false>
 __device__ __forceinline__ void tile_attend(const uint4 (&qr)[KB], const uint4 *__restrict__ Kb,
                                             const uint4 *__restrict__ Vb, int t0, int j1, int sub,
                                             int grp, float *prow, float scale_log2, float (&m)[KB],
-                                            float (&l)[KB], float (&acc)[KB][Geo<D, BF16>::kEpl])
+                                            float (&l)[KB], float (&acc)[KB][Geo<D, BF16>::kEpl],
+                                            const Anc &an = Anc{})
 {
     using G = Geo<D, BF16>;
     constexpr int kEpl = G::kEpl, kLpr = G::kLpr, kRpi = G::kRpi;
@@ -305,8 +328,10 @@ __device__ __forceinline__ void tile_attend(const uint4 (&qr)[KB], const uint4 *
 #pragma unroll
     for (int u = 0; u < kIt; ++u) {
         const int j = min(t0 + u * kRpi + grp, j1 - 1);
-        kr[u] = load_nt(Kb + (size_t)j * kLpr + sub);
-        vr[u] = load_nt(Vb + (size_t)j * kLpr + sub);
+        size_t at = (size_t)j * kLpr + sub;
+        if constexpr (IND) at += (size_t)an.beam_at(t0, u, j) * (an.stride / 16);
+        kr[u] = load_nt(Kb + at);
+        vr[u] = load_nt(Vb + at);
     }
     // QK^T: partial dots of this lane's slice, then a reduce-scatter in the
     // row group, after which the lane owns whole score rows.
@@ -427,11 +452,12 @@ struct ValuTile {
             for (int e = 0; e < kEpl; ++e) s.acc[i][e] = 0.f;
         }
     }
+    template <bool IND = false>
     static __device__ __forceinline__ void attend(const Q &q, const uint4 *__restrict__ Kb,
                                                   const uint4 *__restrict__ Vb, int t0, int j1, int lane,
-                                                  void *lds, float scale_log2, St &s) {
-        tile_attend<D, BF16, KB>(q.r, Kb, Vb, t0, j1, lane % kLpr, lane / kLpr, static_cast<float *>(lds),
-                                 scale_log2, s.m, s.l, s.acc);
+                                                  void *lds, float scale_log2, St &s, const Anc &an = Anc{}) {
+        tile_attend<D, BF16, KB, IND>(q.r, Kb, Vb, t0, j1, lane % kLpr, lane / kLpr, static_cast<float *>(lds),
+                                      scale_log2, s.m, s.l, s.acc, an);
     }
     // this wave's state into LDS: m_w[KB], l_w[KB], a_w[KB][D]
     static __device__ __forceinline__ void to_lds(const St &s, int lane, float *m_w, float *l_w, float *a_w) {
@@ -548,9 +574,10 @@ struct MfmaTile {
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    template <bool IND = false>
     static __device__ __forceinline__ void attend(const Q &q, const uint4 *__restrict__ Kb,
                                                   const uint4 *__restrict__ Vb, int t0, int j1, int lane,
-                                                  void *lds, float scale_log2, St &st) {
+                                                  void *lds, float scale_log2, St &st, const Anc &an = Anc{}) {
         const int n = lane & 15, g = lane >> 4;
         // Row loads in the coalesced layout: kLpr lanes per row, so one
         // instruction reads whole rows (loads of 16 half rows each are
@@ -560,13 +587,30 @@ struct MfmaTile {
         // through LDS can start while V is in flight.
         constexpr int kRpi = kWave / kLpr;
         const int sub = lane % kLpr, grp = lane / kLpr;
-        const auto kres = row_rsrc(Kb, j1 * 2 * D), vres = row_rsrc(Vb, j1 * 2 * D);
-        const int off = ((t0 + grp) * kLpr + sub) * 16;
         uint4 kr[kIt], vr[kIt];
+        if constexpr (!IND) {
+            const auto kres = row_rsrc(Kb, j1 * 2 * D), vres = row_rsrc(Vb, j1 * 2 * D);
+            const int off = ((t0 + grp) * kLpr + sub) * 16;
 #pragma unroll
-        for (int u = 0; u < kIt; ++u) kr[u] = load_rows(kres, off, u * kRpi * 2 * D);
+            for (int u = 0; u < kIt; ++u) kr[u] = load_rows(kres, off, u * kRpi * 2 * D);
 #pragma unroll
-        for (int u = 0; u < kIt; ++u) vr[u] = load_rows(vres, off, u * kRpi * 2 * D);
+            for (int u = 0; u < kIt; ++u) vr[u] = load_rows(vres, off, u * kRpi * 2 * D);
+        } else {
+            // each row from its beam's block; rows at or past j1 get an
+            // offset past the range and read zero without a memory access
+            const auto kres = row_rsrc(Kb, an.k * an.stride), vres = row_rsrc(Vb, an.k * an.stride);
+            int off[kIt];
+#pragma unroll
+            for (int u = 0; u < kIt; ++u) {
+                const int j = t0 + grp + u * kRpi;
+                const int a = an.beam_at(t0, u, min(j, j1 - 1));
+                off[u] = j < j1 ? a * an.stride + (j * kLpr + sub) * 16 : 0x7ffffff0;
+            }
+#pragma unroll
+            for (int u = 0; u < kIt; ++u) kr[u] = load_rows(kres, off[u], 0);
+#pragma unroll
+            for (int u = 0; u < kIt; ++u) vr[u] = load_rows(vres, off[u], 0);
+        }
         // K through LDS into the MFMA A layout: lane l takes row 16 kb + n,
         // dims 32 s + 8 g .. + 8
         char *vt = static_cast<char *>(lds);
@@ -766,17 +810,16 @@ struct GenState {
 // state.  Each tile's state passes through the wave's LDS area (m, l, then
 // acc[D] at float 4), so the running state takes a few registers per lane
 // rather than a whole tile state.
-template <int D, bool BF16>
-__device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
-                                                const uint4 *__restrict__ Vt, size_t hyp, int h, int H, int T,
-                                                int t, int lane, void *lds, float scale_log2, GenState<D> &gs)
+template <int D, bool BF16, bool IND>
+__device__ __forceinline__ void generated_fold(const uint4 *__restrict__ q, const uint4 *__restrict__ Kb,
+                                               const uint4 *__restrict__ Vb, size_t hyp, int h, int H, int t,
+                                               int lane, void *lds, float scale_log2, GenState<D> &gs,
+                                               const Anc &an)
 {
     using TL = Tile<D, BF16, 1>;
-    constexpr int kLpr = Geo<D, BF16>::kLpr, kTile = Geo<D, BF16>::kTile, kE = GenState<D>::kE;
+    constexpr int kTile = Geo<D, BF16>::kTile, kE = GenState<D>::kE;
     typename TL::Q qv;
     TL::load_q(qv, q, hyp, h, H, lane);
-    const uint4 *Kb = Kt + (hyp * H + h) * (size_t)T * kLpr;
-    const uint4 *Vb = Vt + (hyp * H + h) * (size_t)T * kLpr;
     float *slot = static_cast<float *>(lds);
     gs.m = -INFINITY;
     gs.l = 0.f;
@@ -784,7 +827,7 @@ __device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, con
     for (int e = 0; e < kE; ++e) gs.a[e] = 0.f;
     for (int t0 = 0; t0 < t; t0 += kTile) {
         typename TL::St ts;
-        TL::attend(qv, Kb, Vb, t0, t, lane, lds, scale_log2, ts);
+        TL::template attend<IND>(qv, Kb, Vb, t0, t, lane, lds, scale_log2, ts, an);
         TL::to_lds(ts, lane, slot, slot + 1, slot + 4);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
@@ -809,14 +852,40 @@ __device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, con
     }
 }
 
+// Beam `self` of a source, hypothesis hyp = source * k + self: its state over
+// its generated rows [0, t) of head h.  Without a table they are rows of its
+// own block of Kt/Vt; with an ancestry row (anc_row[j] = the beam whose block
+// holds its row j) each row comes from that beam's block.
+template <int D, bool BF16, bool ANC>
+__device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
+                                                const uint4 *__restrict__ Vt, size_t hyp, int h, int H, int T,
+                                                int t, int lane, void *lds, float scale_log2, GenState<D> &gs,
+                                                const int32_t *anc_row, int self, int k,
+                                                const int (&first)[kIt] = {}, bool early = false)
+{
+    constexpr int kLpr = Geo<D, BF16>::kLpr;
+    if constexpr (ANC) {
+        const size_t base = ((hyp - self) * H + h) * (size_t)T * kLpr;   // the source's beam-0 block
+        Anc an{anc_row, self, k, H * T * kLpr * 16};
+        an.early = early;
+#pragma unroll
+        for (int u = 0; u < kIt; ++u) an.first[u] = first[u];
+        generated_fold<D, BF16, true>(q, Kt + base, Vt + base, hyp, h, H, t, lane, lds, scale_log2, gs, an);
+    } else {
+        const size_t base = (hyp * H + h) * (size_t)T * kLpr;
+        generated_fold<D, BF16, false>(q, Kt + base, Vt + base, hyp, h, H, t, lane, lds, scale_log2, gs, Anc{});
+    }
+}
+
 // Generated-token segment of (b, h) = bh (SPLIT only): wave w attends beam
 // i = w, w + 4, ... over that hypothesis' own rows [0, t) of Kt/Vt and stores
 // the beam's state in record slot NC of (b, h).
-template <int D, bool BF16, int KB>
+template <int D, bool BF16, int KB, bool ANC>
 __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                  const uint4 *__restrict__ Vt, unsigned long long *__restrict__ part,
                                                  int bh, int n_bh, int H, int NC, int T, int t,
-                                                 float scale_log2, unsigned long long epoch, void *lds)
+                                                 float scale_log2, unsigned long long epoch, void *lds,
+                                                 const int32_t *__restrict__ anc, int ld_anc)
 {
     if (bh >= n_bh || t <= 0) return;
     const int b = bh / H;
@@ -828,7 +897,9 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
     for (int i = w; i < KB; i += kWaves) {
         GenState<D> gs;
-        generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, lds, scale_log2, gs);
+        const size_t hyp = (size_t)b * KB + i;
+        generated_state<D, BF16, ANC>(q, Kt, Vt, hyp, h, H, T, t, lane, lds, scale_log2, gs,
+                                      ANC ? anc + hyp * ld_anc : nullptr, i, KB);
 #pragma unroll
         for (int e = 0; e < GenState<D>::kE; ++e) {
             const int d = lane + e * kWave;
@@ -841,13 +912,14 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     }
 }
 
-template <int D, bool BF16, int KB, bool SPLIT>
+template <int D, bool BF16, int KB, bool SPLIT, bool ANC = false>
 __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
     const int32_t *__restrict__ src_len, void *__restrict__ out,
     unsigned long long *__restrict__ part,
     int n_bh, int H, int S, int NC, float scale_log2, unsigned long long epoch,
-    const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t)
+    const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t, const int32_t *__restrict__ anc,
+    int ld_anc)
 {
     using G = Geo<D, BF16>;
     using TL = Tile<D, BF16, KB>;
@@ -868,8 +940,8 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     int g = blockIdx.x;
     if constexpr (SPLIT) {
         if (g < n_bh8) {
-            attend_generated<D, BF16, KB>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
-                                          &t_lds[wave_id()][0]);
+            attend_generated<D, BF16, KB, ANC>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
+                                          &t_lds[wave_id()][0], anc, ld_anc);
             return;
         }
         g -= n_bh8;
@@ -952,11 +1024,12 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
 // order, the chunk states folded in chunk order from the empty state, the
 // generated-token state last -- so both kernels give the same bits.  It pays
 // when there are enough (b, h) rows to fill the chip without splitting them.
-template <int D, bool BF16, int KB, bool SPLIT, int P>
+template <int D, bool BF16, int KB, bool SPLIT, int P, bool ANC = false>
 __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
     const int32_t *__restrict__ src_len, void *__restrict__ out, int n_bh, int H, int S,
-    float scale_log2, const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t)
+    float scale_log2, const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t,
+    const int32_t *__restrict__ anc, int ld_anc)
 {
     using G = Geo<D, BF16>;
     using TL = Tile<D, BF16, KB>;
@@ -984,6 +1057,24 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const int lane = tid & (kWave - 1);
     const int w = wave_id();
     const size_t obase = ((size_t)b * KB * H + h) * D;  // out[b, 0, h, 0]
+    // Through an ancestry table, the waves that take the generated-token job
+    // (first group, round 0) load the beams of their first tile's rows now,
+    // alongside src_len, instead of in front of the tile's K/V loads.
+    int first[kIt] = {};
+    bool early = false;
+    if constexpr (SPLIT && ANC) {
+        const int wg = wave_id();
+        if (t > 0 && wg < kWaves && wg < KB) {
+            const int32_t *row = anc + ((size_t)b * KB + wg) * ld_anc;
+            const int grp = (int)(threadIdx.x & (kWave - 1)) / kLpr;
+#pragma unroll
+            for (int u = 0; u < kIt; ++u) {
+                const int a = row[min(grp + u * G::kRpi, t - 1)];
+                first[u] = (a >= 0 && a < KB) ? a : wg;
+            }
+            early = true;
+        }
+    }
 
     typename TL::Q qv;
     TL::load_q(qv, q, (size_t)b * KB, h, H, lane);
@@ -1004,26 +1095,33 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const int njobs = nc + ng;
     const int cg = w / kWaves;   // group of this wave: job j0 + cg of each step
     const int wt = w % kWaves;   // its wave in the group
+
+    // The first group takes the generated-token job (job 0 of round 0) here,
+    // before the job loop: its state stays out of the loop's registers (and
+    // beams loaded early from an ancestry table die before it).
+    if constexpr (SPLIT) {
+        if (ng && cg == 0) {
+            for (int i = wt; i < KB; i += kWaves) {
+                GenState<D> gs;
+                const size_t hyp = (size_t)b * KB + i;
+                generated_state<D, BF16, ANC>(q, Kt, Vt, hyp, h, H, T, t, lane, &t_lds[w][0], scale_log2, gs,
+                                              ANC ? anc + hyp * ld_anc : nullptr, i, KB, first, early && i == wt);
+#pragma unroll
+                for (int e = 0; e < GenState<D>::kE; ++e) {
+                    const int d = lane + e * kWave;
+                    if (d < D) g_lds[i][d] = gs.a[e];
+                }
+                if (lane == 0) {
+                    gm_lds[i] = gs.m;
+                    gl_lds[i] = gs.l;
+                }
+            }
+        }
+    }
     for (int j0 = 0; j0 < njobs; j0 += P) {
         const int c = j0 + cg - ng;  // chunk of this group's job; -1: generated tokens
         if (j0 + cg < njobs && c < 0) {
-            if constexpr (SPLIT) {
-                // beam i's state over its own generated rows
-                for (int i = wt; i < KB; i += kWaves) {
-                    GenState<D> gs;
-                    generated_state<D, BF16>(q, Kt, Vt, (size_t)b * KB + i, h, H, T, t, lane, &t_lds[w][0],
-                                             scale_log2, gs);
-#pragma unroll
-                    for (int e = 0; e < GenState<D>::kE; ++e) {
-                        const int d = lane + e * kWave;
-                        if (d < D) g_lds[i][d] = gs.a[e];
-                    }
-                    if (lane == 0) {
-                        gm_lds[i] = gs.m;
-                        gl_lds[i] = gs.l;
-                    }
-                }
-            }
+            // the generated-token job, already taken before this loop
         } else if (j0 + cg < njobs) {
             typename TL::St st;
             TL::init(st);
@@ -1084,12 +1182,14 @@ struct AttnArgs {
     int B, k, H, S, D;
     const void *Kt, *Vt;
     int T, t;
+    const int32_t *anc;   // ancestry table of the generated rows, or null
+    int ld_anc;
     float *ws;
     unsigned long long epoch;
     hipStream_t stream;
 };
 
-template <int D, bool BF16, int KB, bool SPLIT>
+template <int D, bool BF16, int KB, bool SPLIT, bool ANC = false>
 hipError_t launch_split(const AttnArgs &a, int NC)
 {
     const int n_bh = a.B * a.H;
@@ -1099,23 +1199,24 @@ hipError_t launch_split(const AttnArgs &a, int NC)
     // [generated-token workgroups] [chunk workgroups] [mergers]
     const long long mergers = (SPLIT || NC > 1) ? n_bh : 0;
     const long long nblk = (SPLIT ? n_bh8 : 0) + n_bh8 * NC + mergers;
-    hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB, SPLIT>), dim3((unsigned)nblk), dim3(kBlock), 0,
+    hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB, SPLIT, ANC>), dim3((unsigned)nblk), dim3(kBlock), 0,
                        a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
                        static_cast<const uint4 *>(a.V), a.src_len, a.out, part, n_bh, a.H, a.S,
                        NC, (float)scale_log2, a.epoch, static_cast<const uint4 *>(a.Kt),
-                       static_cast<const uint4 *>(a.Vt), a.T, a.t);
+                       static_cast<const uint4 *>(a.Vt), a.T, a.t, a.anc, a.ld_anc);
     return hipGetLastError();
 }
 
-template <int D, bool BF16, int KB, bool SPLIT, int P>
+template <int D, bool BF16, int KB, bool SPLIT, int P, bool ANC = false>
 hipError_t launch_whole(const AttnArgs &a)
 {
     const int n_bh = a.B * a.H;
     const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
-    hipLaunchKernelGGL((attn_whole_kernel<D, BF16, KB, SPLIT, P>), dim3((unsigned)n_bh), dim3(kBlock * P), 0,
+    hipLaunchKernelGGL((attn_whole_kernel<D, BF16, KB, SPLIT, P, ANC>), dim3((unsigned)n_bh), dim3(kBlock * P), 0,
                        a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
                        static_cast<const uint4 *>(a.V), a.src_len, a.out, n_bh, a.H, a.S, (float)scale_log2,
-                       static_cast<const uint4 *>(a.Kt), static_cast<const uint4 *>(a.Vt), a.T, a.t);
+                       static_cast<const uint4 *>(a.Kt), static_cast<const uint4 *>(a.Vt), a.T, a.t, a.anc,
+                       a.ld_anc);
     return hipGetLastError();
 }
 
@@ -1127,7 +1228,20 @@ hipError_t launch_typed(const AttnArgs &a)
     // S == 0) still has a workgroup to write its zero output
     const int NC = max(1, (a.S + G::kChunk - 1) / G::kChunk);
     // jobs per row: its chunks, plus the generated tokens of the split cache
-    switch (choose_attn_path(a.B * a.H, NC + (SPLIT && a.t > 0 ? 1 : 0))) {
+    const AttnPath path = choose_attn_path(a.B * a.H, NC + (SPLIT && a.t > 0 ? 1 : 0));
+    if constexpr (SPLIT) {
+        if (a.anc) {
+            // generated rows through the ancestry table: their own kernels,
+            // so that the table-free ones keep their registers
+            switch (path) {
+            case AttnPath::kWhole1: return launch_whole<D, BF16, KB, true, 1, true>(a);
+            case AttnPath::kWhole2: return launch_whole<D, BF16, KB, true, 2, true>(a);
+            case AttnPath::kWhole4: return launch_whole<D, BF16, KB, true, 4, true>(a);
+            default: return launch_split<D, BF16, KB, true, true>(a, NC);
+            }
+        }
+    }
+    switch (path) {
     case AttnPath::kWhole1: return launch_whole<D, BF16, KB, SPLIT, 1>(a);
     case AttnPath::kWhole2: return launch_whole<D, BF16, KB, SPLIT, 2>(a);
     case AttnPath::kWhole4: return launch_whole<D, BF16, KB, SPLIT, 4>(a);
@@ -1204,16 +1318,16 @@ hipError_t launch_cross_attn(const void *q, const void *K, const void *V, const 
                              void *out, int B, int k, int H, int S, int D, bool bf16,
                              float *workspace, unsigned long long epoch, hipStream_t stream)
 {
-    const AttnArgs a{q, K, V, src_len, out, B, k, H, S, D, nullptr, nullptr, 0, 0, workspace, epoch, stream};
+    const AttnArgs a{q, K, V, src_len, out, B, k, H, S, D, nullptr, nullptr, 0, 0, nullptr, 0, workspace, epoch, stream};
     return bf16 ? launch_d<true, false>(a) : launch_d<false, false>(a);
 }
 
 hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
-                              const void *Kt, const void *Vt, int T, int t, void *out, int B, int k,
-                              int H, int N, int D, bool bf16, float *workspace,
+                              const void *Kt, const void *Vt, int T, int t, const int32_t *anc, int ld_anc,
+                              void *out, int B, int k, int H, int N, int D, bool bf16, float *workspace,
                               unsigned long long epoch, hipStream_t stream)
 {
-    const AttnArgs a{q, Kp, Vp, prefix_len, out, B, k, H, N, D, Kt, Vt, T, t, workspace, epoch, stream};
+    const AttnArgs a{q, Kp, Vp, prefix_len, out, B, k, H, N, D, Kt, Vt, T, t, anc, ld_anc, workspace, epoch, stream};
     return bf16 ? launch_d<true, true>(a) : launch_d<false, true>(a);
 }
 

@@ -41,9 +41,11 @@ hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
 
 // Split-cache self-attention: shared prefix Kp/Vp [B,H,N,D] with
 // prefix_len[B], per-beam generated tokens Kt/Vt [B*k,H,T,D] (rows < t).
+// anc: [B*k, ld_anc] int32 ancestry table of the generated rows, or null
+// (each hypothesis reads its own rows).
 hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
-                              const void *Kt, const void *Vt, int T, int t, void *out, int B, int k,
-                              int H, int N, int D, bool bf16, float *workspace,
+                              const void *Kt, const void *Vt, int T, int t, const int32_t *anc, int ld_anc,
+                              void *out, int B, int k, int H, int N, int D, bool bf16, float *workspace,
                               unsigned long long epoch, hipStream_t stream);
 
 hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t,
@@ -66,5 +68,8 @@ hipError_t launch_beam_select(const float *logits, const float *beam_scores, con
 int cache_reorder_chunk(const void *K, const void *V, int T, int t, int D, int esize);
 hipError_t launch_cache_reorder(void *K, void *V, const int32_t *parent, int B, int k, int H, int T, int t, int D,
                                 int esize, hipStream_t stream);
+// Ancestry table step: columns < t from the parents, column t the own index.
+hipError_t launch_ancestry_step(int32_t *anc, int ld, const int32_t *parent, int B, int k, int t,
+                                hipStream_t stream);
 
 }  // namespace fs

@@ -96,6 +96,26 @@ static PyObject *py_cache_reorder(PyObject *self, PyObject *const *args, Py_ssiz
     return PyLong_FromLong(st);
 }
 
+static PyObject *py_ancestry_step(PyObject *self, PyObject *const *args, Py_ssize_t nargs) {
+    unsigned long long u[7];
+    int v[7];
+    (void)self;
+    if (unpack(args, nargs, "pipiiip", u, v)) return NULL;
+    int st = fs_beam_ancestry_step((int32_t *)PTR(0), v[1], (const int32_t *)PTR(2), v[3], v[4], v[5], PTR(6));
+    return PyLong_FromLong(st);
+}
+
+static PyObject *py_beam_prefix_attn_indirect(PyObject *self, PyObject *const *args, Py_ssize_t nargs) {
+    unsigned long long u[20];
+    int v[20];
+    (void)self;
+    if (unpack(args, nargs, "pppppppiiipiiiiiippp", u, v)) return NULL;
+    int st = fs_beam_prefix_attn_indirect(PTR(0), PTR(1), PTR(2), (const int32_t *)PTR(3), PTR(4), PTR(5),
+                                          (const int32_t *)PTR(6), v[7], v[8], v[9], PTR(10), v[11], v[12], v[13],
+                                          v[14], v[15], v[16], PTR(17), (size_t)u[18], PTR(19));
+    return PyLong_FromLong(st);
+}
+
 static PyObject *py_last_error(PyObject *self, PyObject *unused) {
     (void)self;
     (void)unused;
@@ -115,6 +135,11 @@ static PyMethodDef methods[] = {
      "workspace, workspace_bytes, stream)"},
     {"fs_cache_reorder", (PyCFunction)(void (*)(void))py_cache_reorder, METH_FASTCALL,
      "fs_cache_reorder(K, V, parent, B, k, H, T, t, D, dtype, stream)"},
+    {"fs_beam_ancestry_step", (PyCFunction)(void (*)(void))py_ancestry_step, METH_FASTCALL,
+     "fs_beam_ancestry_step(anc, ld_anc, parent, B, k, t, stream)"},
+    {"fs_beam_prefix_attn_indirect", (PyCFunction)(void (*)(void))py_beam_prefix_attn_indirect, METH_FASTCALL,
+     "fs_beam_prefix_attn_indirect(q, Kp, Vp, prefix_len, Kt, Vt, anc, ld_anc, T, t, out, B, k, H, N, D, dtype, "
+     "workspace, workspace_bytes, stream)"},
     {"fs_last_error", py_last_error, METH_NOARGS, "fs_last_error() -> str"},
     {NULL, NULL, 0, NULL},
 };

@@ -307,3 +307,25 @@ def reorder_inputs(cfg) -> dict:
     parent = np.floor(cfg.k * rng.random(cfg.B * cfg.k) ** 2).astype(np.int32)
     return {"parent": parent, "B": cfg.B, "k": cfg.k, "H": cfg.H, "T": cfg.t, "t": cfg.t, "D": cfg.D,
             "dtype": cfg.dtype}
+
+
+def ancestry_inputs(cfg) -> dict:
+    """An ancestry table and parents for the split-cache workload.
+
+    anc [B*k, T] int32: for each hypothesis and generated position tau < t,
+    the beam (within its source) whose row holds that token, floor(k * u^2)
+    with u ~ U[0, 1) (favouring the best beams, every position drawn on its
+    own: few rows come from the hypothesis' own block); positions tau >= t
+    hold the hypothesis' own index.  parent [B*k]: the same law, for a
+    reorder of the same cache.  Streams SeedSequence([210604718, cfg, 3000])
+    and [.., 3001].
+    """
+    if isinstance(cfg, str):
+        cfg = PREFIX_CONFIGS[cfg]
+    rows = cfg.B * cfg.k
+    rng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, cfg.index, 3000]))
+    anc = np.tile((np.arange(rows) % cfg.k).astype(np.int32)[:, None], (1, cfg.T))
+    anc[:, :cfg.t] = np.floor(cfg.k * rng.random((rows, cfg.t)) ** 2).astype(np.int32)
+    prng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, cfg.index, 3001]))
+    parent = np.floor(cfg.k * prng.random(rows) ** 2).astype(np.int32)
+    return {"anc": anc, "parent": parent}

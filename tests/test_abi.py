@@ -229,3 +229,51 @@ def test_reorder_nothing_to_move_returns_ok_without_launch():
     E = N.ext()
     assert E.fs_cache_reorder(FAKE, FAKE, FAKE * 128, 2, 4, 2, 10, 5, 16, N.FS_BF16, None) == N.FS_ERR_INVALID_ARG
     assert "K overlaps V" in E.fs_last_error()
+
+
+def ancestry(**kw):
+    a = dict(anc=FAKE, ld=10, parent=FAKE * 64, B=2, k=4, t=3, stream=None)
+    a.update(kw)
+    return N.lib().fs_beam_ancestry_step(a["anc"], a["ld"], a["parent"], a["B"], a["k"], a["t"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(t=10), N.FS_ERR_INVALID_ARG, "column t=10"),
+    (dict(B=-1), N.FS_ERR_INVALID_ARG, "negative"),
+    (dict(k=17), N.FS_ERR_UNSUPPORTED, "k=17"),
+    (dict(anc=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(parent=FAKE * 64 + 2), N.FS_ERR_INVALID_ARG, "aligned"),
+    (dict(parent=FAKE + 8), N.FS_ERR_INVALID_ARG, "overlaps"),
+])
+def test_ancestry_rejects(kw, status, needle):
+    assert ancestry(**kw) == status
+    assert needle in N.last_error()
+    assert ancestry(B=0, anc=None, parent=None) == N.FS_OK
+
+
+def indirect(**kw):
+    a = dict(q=FAKE, Kp=FAKE * 2, Vp=FAKE * 3, plen=FAKE * 4, Kt=FAKE * 5, Vt=FAKE * 6, anc=FAKE * 7, ld=8,
+             T=8, t=5, out=FAKE * 9, B=2, k=4, H=2, N=16, D=64, dtype=N.FS_BF16, ws=FAKE * 10, wsb=1 << 24,
+             stream=None)
+    a.update(kw)
+    return N.lib().fs_beam_prefix_attn_indirect(a["q"], a["Kp"], a["Vp"], a["plen"], a["Kt"], a["Vt"], a["anc"],
+                                                a["ld"], a["T"], a["t"], a["out"], a["B"], a["k"], a["H"], a["N"],
+                                                a["D"], a["dtype"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(anc=None), N.FS_ERR_INVALID_ARG, "null ancestry table"),
+    (dict(ld=4), N.FS_ERR_INVALID_ARG, "ld_anc=4 < t=5"),
+    (dict(anc=FAKE * 7 + 2), N.FS_ERR_INVALID_ARG, "anc must be 4-byte aligned"),
+    (dict(anc=FAKE * 9 + 16), N.FS_ERR_INVALID_ARG, "out overlaps the ancestry table"),
+    (dict(t=9), N.FS_ERR_INVALID_ARG, "exceeds"),
+    (dict(D=48), N.FS_ERR_UNSUPPORTED, "D=48"),
+])
+def test_indirect_prefix_attn_rejects(kw, status, needle):
+    assert indirect(**kw) == status
+    assert needle in N.last_error()
+
+
+def test_indirect_prefix_attn_needs_no_table_without_generated_tokens():
+    # t == 0 reads no table: a null anc passes validation (and B == 0 launches nothing)
+    assert indirect(anc=None, t=0, B=0) == N.FS_OK

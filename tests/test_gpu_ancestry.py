@@ -1,0 +1,160 @@
+"""GPU parity of the reorder-free cache maintenance: fs_beam_ancestry_step
+against the oracle (bit-exact integers), and fs_beam_prefix_attn_indirect
+(the split-cache attention reading its generated rows through the table)
+against the fp64 oracle and, bit for bit, against fs_beam_prefix_attn on the
+physically reordered cache.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2106_04718_amd import api, workloads
+
+from _gpu import assert_attn_close, bits, device, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def random_parents(rows, k, rng, bad=0.0):
+    p = rng.integers(0, k, size=rows).astype(np.int32)
+    if bad:
+        m = rng.random(rows) < bad
+        p[m] = rng.choice(np.array([-1, k, 1 << 20], np.int32), size=int(m.sum()))
+    return p
+
+
+@pytest.mark.parametrize("k", [1, 2, 4, 5, 8, 16])
+def test_ancestry_steps_match_the_oracle(k):
+    dev = device()
+    rng = np.random.default_rng(k)
+    B, ld = 7, 300
+    anc_h = rng.integers(-3, 40, size=(B * k, ld)).astype(np.int32)
+    anc = torch.from_numpy(anc_h.copy()).to(dev)
+    for t in (0, 1, 2, 63, 64, 255, 256, 299):
+        say(f"[ancestry] k={k} t={t}")
+        p = random_parents(B * k, k, rng, bad=0.1)
+        api.ancestry_step(anc, torch.from_numpy(p).to(dev), k, t)
+        anc_h = oracle.ancestry_step(anc_h, p, k, t)
+        torch.cuda.synchronize()
+        assert np.array_equal(anc.cpu().numpy(), anc_h), f"k={k} t={t}"
+
+
+def decode(B, k, H, N, T, D, dtype, steps, seed, plen):
+    """A simulated decode on the GPU: per step a selection (random parents),
+    then the physical reorder of one cache and the table step of the other,
+    then the step's new K/V appended to each hypothesis' own row of both."""
+    dev = device()
+    rng = np.random.default_rng(seed)
+
+    def draw(shape):
+        x = rng.standard_normal(shape).astype(np.float32)
+        return x if dtype == "f32" else workloads.f32_to_bf16_bits(x)
+
+    q, Kp, Vp = to_dev(draw((B, k, H, D))), to_dev(draw((B, H, N, D))), to_dev(draw((B, H, N, D)))
+    pl = torch.from_numpy(np.asarray(plen, np.int32)).to(dev)
+    z = to_dev(draw((B * k, H, T, D))) * 0
+    Kr, Vr = z.clone(), z.clone()          # physically reordered
+    Ki, Vi = z.clone(), z.clone()          # never moved, read through the table
+    anc = torch.zeros((B * k, T), dtype=torch.int32, device=dev)
+    parents = []
+    for t in range(steps):
+        p = torch.from_numpy(random_parents(B * k, k, rng, bad=0.05)).to(dev)
+        parents.append(p.cpu().numpy())
+        api.cache_reorder(Kr, Vr, p, k, t)
+        api.ancestry_step(anc, p, k, t)
+        nk, nv = to_dev(draw((B * k, H, D))), to_dev(draw((B * k, H, D)))
+        Kr[:, :, t] = nk
+        Vr[:, :, t] = nv
+        Ki[:, :, t] = nk
+        Vi[:, :, t] = nv
+    torch.cuda.synchronize()
+    return dict(q=q, Kp=Kp, Vp=Vp, pl=pl, Kr=Kr, Vr=Vr, Ki=Ki, Vi=Vi, anc=anc, t=steps)
+
+
+@pytest.mark.parametrize("dtype,D,k", [("bf16", 64, 4), ("bf16", 128, 5), ("f32", 32, 4), ("bf16", 32, 8),
+                                       ("f32", 16, 2)])
+def test_table_read_equals_the_reordered_cache_bitwise_on_every_path(dtype, D, k):
+    B, H, N, T = 3, 2, 600, 80
+    s = decode(B, k, H, N, T, D, dtype, steps=70, seed=D + k, plen=[600, 0, 257])
+    old = os.environ.get("FS_ATTN_PATH")
+    try:
+        for path in ("split", "whole1", "whole2", "whole4"):
+            os.environ["FS_ATTN_PATH"] = path
+            say(f"[indirect] {dtype} D={D} k={k} path={path}")
+            direct = api.beam_prefix_attn(s["q"], s["Kp"], s["Vp"], s["pl"], s["Kr"], s["Vr"], s["t"])
+            ind = api.beam_prefix_attn(s["q"], s["Kp"], s["Vp"], s["pl"], s["Ki"], s["Vi"], s["t"], anc=s["anc"])
+            torch.cuda.synchronize()
+            assert np.array_equal(bits(direct), bits(ind)), f"path={path}"
+    finally:
+        if old is None:
+            os.environ.pop("FS_ATTN_PATH", None)
+        else:
+            os.environ["FS_ATTN_PATH"] = old
+    want = oracle.prefix_attn_indirect(to_host(s["q"]), to_host(s["Kp"]), to_host(s["Vp"]), s["pl"].cpu().numpy(),
+                                       to_host(s["Ki"]), to_host(s["Vi"]), s["anc"].cpu().numpy(), s["t"])
+    assert_attn_close(ind, want, f"indirect {dtype} D={D} k={k}")
+
+
+def to_host(x):
+    c = x.cpu().contiguous()
+    if c.dtype == torch.bfloat16:
+        return c.view(torch.int16).numpy().view(np.uint16)
+    return c.numpy()
+
+
+def test_gpt2_shaped_decode_against_the_oracle():
+    # the split-cache workload's shape (B=16, k=4, H=12, D=64) with 64 steps of ancestry
+    B, k, H, N, T, D = 16, 4, 12, 400, 64, 64
+    plen = np.random.default_rng(5).integers(100, 401, size=B)
+    s = decode(B, k, H, N, T, D, "bf16", steps=64, seed=11, plen=plen)
+    ind = api.beam_prefix_attn(s["q"], s["Kp"], s["Vp"], s["pl"], s["Ki"], s["Vi"], s["t"], anc=s["anc"])
+    torch.cuda.synchronize()
+    want = oracle.prefix_attn_indirect(to_host(s["q"]), to_host(s["Kp"]), to_host(s["Vp"]), s["pl"].cpu().numpy(),
+                                       to_host(s["Ki"]), to_host(s["Vi"]), s["anc"].cpu().numpy(), s["t"])
+    err = assert_attn_close(ind, want, "gpt2-shaped indirect")
+    say(f"[indirect] gpt2-shaped max_abs_err={err:.3e}")
+
+
+def test_identity_table_gives_the_direct_bits_and_t_zero_reads_no_table():
+    dev = device()
+    B, k, H, N, T, D, t = 4, 4, 3, 300, 50, 64, 37
+    rng = np.random.default_rng(3)
+
+    def draw(shape):
+        return to_dev(workloads.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32)))
+
+    q, Kp, Vp, Kt, Vt = draw((B, k, H, D)), draw((B, H, N, D)), draw((B, H, N, D)), draw((B * k, H, T, D)), \
+        draw((B * k, H, T, D))
+    pl = torch.tensor([300, 1, 0, 150], dtype=torch.int32, device=dev)
+    ident = torch.arange(k, dtype=torch.int32, device=dev).repeat(B)[:, None].expand(B * k, T).contiguous()
+    a = api.beam_prefix_attn(q, Kp, Vp, pl, Kt, Vt, t)
+    b = api.beam_prefix_attn(q, Kp, Vp, pl, Kt, Vt, t, anc=ident)
+    # out-of-range entries read the hypothesis' own row, like the identity
+    wild = ident.clone()
+    wild[:, ::3] = -5
+    c = api.beam_prefix_attn(q, Kp, Vp, pl, Kt, Vt, t, anc=wild)
+    d0 = api.beam_prefix_attn(q, Kp, Vp, pl, Kt, Vt, 0)
+    e0 = api.beam_prefix_attn(q, Kp, Vp, pl, Kt, Vt, 0, anc=torch.zeros((B * k, 1), dtype=torch.int32, device=dev))
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(a), bits(b))
+    assert np.array_equal(bits(a), bits(c))
+    assert np.array_equal(bits(d0), bits(e0))
+
+
+def test_rejects_bad_tables_on_device_tensors():
+    dev = device()
+    B, k, H, N, T, D = 2, 4, 1, 8, 6, 16
+    z = lambda *s: torch.zeros(s, dtype=torch.bfloat16, device=dev)
+    args = (z(B, k, H, D), z(B, H, N, D), z(B, H, N, D), torch.full((B,), 8, dtype=torch.int32, device=dev),
+            z(B * k, H, T, D), z(B * k, H, T, D))
+    with pytest.raises(Exception, match="ld_anc=3 < t=5"):
+        api.beam_prefix_attn(*args, 5, anc=torch.zeros((B * k, 3), dtype=torch.int32, device=dev))
+    anc = torch.zeros((B * k, 4), dtype=torch.int32, device=dev)
+    with pytest.raises(Exception, match="column t=4"):
+        api.ancestry_step(anc, torch.zeros(B * k, dtype=torch.int32, device=dev), k, 4)
+    with pytest.raises(Exception, match="k=17"):
+        api.ancestry_step(torch.zeros((17, 4), dtype=torch.int32, device=dev),
+                          torch.zeros(17, dtype=torch.int32, device=dev), 17, 1)
