@@ -511,7 +511,7 @@ def bench_indirect(args, cfg, dev) -> int:
     copy_gbps = copy_bandwidth(dev)
     log(f"indirect step {step_us:.2f} us = {gbps:.0f} GB/s ({100 * gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s); direct "
         f"{direct_us:.2f} us; the layer's reorder it replaces {reorder_us:.2f} us; ancestry step {anc_us:.2f} us "
-        f"per decode step")
+        f"per decode step (rate of back-to-back single launches)")
     line = {
         "metric": "split-cache self-attention step through an ancestry table, µs and achieved HBM GB/s, GPT2 shape",
         "value": round(gbps, 2),
