@@ -799,9 +799,12 @@ def bench_reorder(args, cfg, dev) -> int:
 
 
 def kernel_source_sha() -> str:
+    """Hash of what the kernels are built from: the sources and the build
+    flags (a stored traffic figure is only used while it matches)."""
     import hashlib
     h = hashlib.sha256()
-    for p in sorted((ROOT / "paper_2106_04718_amd" / "csrc").glob("*")):
+    pkg = ROOT / "paper_2106_04718_amd"
+    for p in [*sorted((pkg / "csrc").glob("*")), pkg / "build.py"]:
         h.update(p.read_bytes())
     return h.hexdigest()[:16]
 

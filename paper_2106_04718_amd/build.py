@@ -24,6 +24,10 @@ ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          # kernel arguments arrive preloaded in SGPRs: the first wave of a
+          # workgroup skips one dependent scalar load before its first
+          # address computation
+          "-mllvm", "-amdgpu-kernarg-preload-count=16",
           "-Wall", "-Wno-unused-command-line-argument",
           f"-I{ROOT / 'include'}", f"-I{CSRC}"]
 
