@@ -433,6 +433,7 @@ struct ValuTile {
     static constexpr int kEpl = G::kEpl, kLpr = G::kLpr;
     static constexpr int kLdsBytes = G::kPStride * KB * 4;  // per wave
     struct Q { uint4 r[KB]; };
+    static constexpr int kAStride = D;  // floats between the beams of a wave's state in LDS
     // m, l wave-uniform; acc[i][e] holds dims sub*kEpl + e in every lane
     struct St { float m[KB], l[KB], acc[KB][kEpl]; };
 
@@ -465,7 +466,7 @@ struct ValuTile {
 #pragma unroll
             for (int i = 0; i < KB; ++i) {
 #pragma unroll
-                for (int e = 0; e < kEpl; ++e) a_w[i * D + lane * kEpl + e] = s.acc[i][e];
+                for (int e = 0; e < kEpl; ++e) a_w[i * kAStride + lane * kEpl + e] = s.acc[i][e];
             }
         }
         if (lane == 0) {
@@ -539,6 +540,10 @@ struct MfmaTile {
     static_assert(KB <= 16, "beams are the 16 columns of the MFMA");
     static_assert(NKB % 2 == 0, "PV takes 32 keys per instruction");
     struct Q { bf16x8_t b[NS]; };
+    // floats between the beams of a wave's state in LDS: the 16 lanes of one
+    // store (one beam each) land on distinct banks (a stride of D puts them
+    // all on the same four banks)
+    static constexpr int kAStride = D + 4;
     // column state of beam n = lane & 15: m, l identical in the column's
     // four lanes; acc[mb][i] holds dim 16 mb + 4 (lane >> 4) + i
     struct St { float m, l; f32x4_t acc[NU]; };
@@ -699,7 +704,8 @@ struct MfmaTile {
         const int n = lane & 15, g = lane >> 4;
         if (n < KB) {
 #pragma unroll
-            for (int mb = 0; mb < NU; ++mb) *reinterpret_cast<f32x4_t *>(a_w + n * D + 16 * mb + 4 * g) = s.acc[mb];
+            for (int mb = 0; mb < NU; ++mb)
+                *reinterpret_cast<f32x4_t *>(a_w + n * kAStride + 16 * mb + 4 * g) = s.acc[mb];
             if (g == 0) {
                 m_w[n] = s.m;
                 l_w[n] = s.l;
@@ -712,12 +718,13 @@ template <int D, bool BF16, int KB>
 using Tile = typename std::conditional<(BF16 && D >= 32), MfmaTile<D, KB>, ValuTile<D, BF16, KB>>::type;
 
 // LDS area of one wave: large enough for a tile of KB beams or of one beam,
-// for the wave's acc[KB][D] once its tile is done, and for one generated-
+// for the wave's acc (KB rows of kAStride floats) once its tile is done, and for one generated-
 // token tile state (m, l, acc[D] at float 4); a 16-byte multiple.
 template <int D, bool BF16, int KB>
 struct WaveLds {
     static constexpr int a = Tile<D, BF16, KB>::kLdsBytes, b = Tile<D, BF16, 1>::kLdsBytes;
-    static constexpr int c = KB * D * 4 > (D + 4) * 4 ? KB * D * 4 : (D + 4) * 4;
+    static constexpr int s = Tile<D, BF16, KB>::kAStride;
+    static constexpr int c = KB * s * 4 > (D + 4) * 4 ? KB * s * 4 : (D + 4) * 4;
     static constexpr int kBytes = ((a > b ? (a > c ? a : c) : (b > c ? b : c)) + 15) / 16 * 16;
 };
 
@@ -990,9 +997,10 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     if (!SPLIT && nc == 1) {
         for (int x = tid; x < KB * D; x += kBlock) {
             const int i = x / D, d = x - i * D;
-            float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * D + d];
+            float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * TL::kAStride + d];
 #pragma unroll
-            for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * D + d]);
+            for (int ww = 1; ww < kWaves; ++ww)
+                merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * TL::kAStride + d]);
             store_out<BF16>(out, obase + (size_t)i * H * D + d, aa / ll);
         }
         return;
@@ -1003,9 +1011,10 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     for (int x = tid; x < KB * D; x += kBlock) {
         const int i = x / D, d = x - i * D;
-        float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * D + d];
+        float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * TL::kAStride + d];
 #pragma unroll
-        for (int ww = 1; ww < kWaves; ++ww) merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * D + d]);
+        for (int ww = 1; ww < kWaves; ++ww)
+            merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * TL::kAStride + d]);
         store_word(rec + x, tag, aa);
         if (d == 0) {
             store_word(rec + KB * D + i, tag, mm);
@@ -1140,11 +1149,11 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
                     if (j0 + g < ng) continue;  // the generated-token job is folded last
                     const int w0 = g * kWaves;
                     const float *a0 = reinterpret_cast<const float *>(&t_lds[w0][0]);
-                    float mm = m_lds[w0][i], ll = l_lds[w0][i], aa = a0[i * D + d];
+                    float mm = m_lds[w0][i], ll = l_lds[w0][i], aa = a0[i * TL::kAStride + d];
 #pragma unroll
                     for (int ww = 1; ww < kWaves; ++ww) {
                         const float *aw = reinterpret_cast<const float *>(&t_lds[w0 + ww][0]);
-                        merge_state(mm, ll, aa, m_lds[w0 + ww][i], l_lds[w0 + ww][i], aw[i * D + d]);
+                        merge_state(mm, ll, aa, m_lds[w0 + ww][i], l_lds[w0 + ww][i], aw[i * TL::kAStride + d]);
                     }
                     merge_state(Rm[p], Rl[p], Ra[p], mm, ll, aa);
                 }
