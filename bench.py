@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--config", default="bart",
                     help="decode step: tiny | bart | t5 | prophetnet | large; "
                          "split-cache self-attention step: gpt2 | tiny_prefix")
-    ap.add_argument("--part", default="step", choices=("step", "select", "reorder", "indirect"),
+    ap.add_argument("--part", default="step", choices=("step", "select", "reorder", "indirect", "sweep"),
                     help="step: the decode step (cross-attention + n-gram blocking); "
                          "select: the beam-selection step on the same config's logits")
     ap.add_argument("--rounds", type=int, default=5,
@@ -189,6 +189,8 @@ def main() -> int:
         return bench_select(args, workloads.get(args.config), dev)
     if args.part == "reorder":
         return bench_reorder(args, workloads.get(args.config), dev)
+    if args.part == "sweep":
+        return bench_sweep(args, workloads.get(args.config), dev)
     cfg = workloads.get(args.config)
     tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
 
@@ -314,6 +316,118 @@ def main() -> int:
     if not args.no_cpu_baseline:
         line["cpu_baseline"], line["parity"] = cpu_baseline(cfg, base, g, out0, logits0, b_step,
                                                              args.cpu_reps)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def bench_sweep(args, cfg, dev) -> int:
+    """The decode step over the prefix lengths t = 1 .. cfg.t of one token
+    buffer (ld = cfg.t; step t reads its first t columns), at the config's
+    full batch.  The cross-attention does not depend on t; at every t the
+    step (cross-attention then n-gram) is timed against the cross-attention
+    alone, in alternating regions of K steps."""
+    import numpy as np
+    import torch
+
+    from paper_2106_04718_amd import api, workloads
+
+    def dev_tensor(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    tdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    t0 = time.perf_counter()
+    base = workloads.attn_inputs(cfg)
+    lens = base["src_len"]
+    set_bytes = 2 * cfg.B * cfg.H * cfg.S * cfg.D * cfg.esize
+    R = max(1, math.ceil(args.rotate_gib * (1 << 30) / set_bytes))
+    q, lens_d = dev_tensor(base["q"]), dev_tensor(lens)
+    Ks, Vs = [dev_tensor(base["K"])], [dev_tensor(base["V"])]
+    for r in range(1, R):
+        d = workloads.attn_inputs(cfg, rep=r)
+        Ks.append(dev_tensor(d["K"]))
+        Vs.append(dev_tensor(d["V"]))
+        del d
+    del base
+    g = workloads.ngram_inputs(cfg)
+    tokens_d, logits0 = dev_tensor(g["tokens"]), dev_tensor(g["logits"])
+    del g
+    logits_d = torch.empty_like(logits0)
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_cross_attn_workspace_bytes(cfg.B, cfg.k, cfg.H, cfg.S, cfg.D, tdt), dev)
+    torch.cuda.synchronize()
+    log(f"config={cfg.name} sweep: K/V sets={R} ({R * set_bytes / 2**30:.2f} GiB), t = 1..{cfg.t}, "
+        f"inputs ready in {time.perf_counter() - t0:.1f}s")
+    stream = torch.cuda.current_stream(dev)
+    K_ = args.steps
+
+    def region_us(fn) -> float:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(K_):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / K_
+
+    def ca_only(i: int):
+        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
+
+    logits_d.copy_(logits0)
+    for i in range(args.warmup):
+        ca_only(i)
+        api.ngram_block(tokens_d, cfg.n, logits_d)
+    b_ca = attn_bytes(cfg, lens)
+    rows = []
+    for t in range(1, cfg.t + 1):
+        logits_d.copy_(logits0)
+        tok_t = tokens_d[:, :t]
+        api.ngram_block(tok_t, cfg.n, logits_d)
+        bans = int(torch.isneginf(logits_d).sum().item())
+
+        def step(i: int, tok_t=tok_t):
+            ca_only(i)
+            api.ngram_block(tok_t, cfg.n, logits_d)
+
+        a_us, b_us = region_us(step), region_us(ca_only)
+        b_step = b_ca + ngram_bytes(cfg.rows, t, bans)
+        rows.append({"t": t, "step_us": round(a_us, 3), "cross_attn_us": round(b_us, 3),
+                     "ngram_us": round(max(a_us - b_us, 0.0), 3), "bans": bans,
+                     "step_gbps": round(b_step / (a_us * 1e-6) / 1e9, 1)})
+        if t in (1, 2, 4, 8, 16, 32, 64, 96, 128, cfg.t):
+            r = rows[-1]
+            log(f"t={t:3d}: step {r['step_us']:.2f} us = {r['step_gbps']:.0f} GB/s; cross-attn {r['cross_attn_us']:.2f} us; "
+                f"n-gram {r['ngram_us']:.2f} us ({bans} bans)")
+    ca = float(np.median([r["cross_attn_us"] for r in rows]))
+    ca_gbps = b_ca / (ca * 1e-6) / 1e9
+    last = rows[-1]
+    line = {
+        "metric": "decode-step µs and achieved HBM GB/s (cross-attn + n-gram block) over the prefix-length sweep",
+        "value": last["step_gbps"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K_,
+        "warmup": args.warmup,
+        "ms_per_step": round(last["step_us"] * 1e-3, 6),
+        "step_us": last["step_us"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded; BART-large-shaped K/V, Zipf(1.1) token prefixes)",
+        "config": {"workload": workload_name(cfg) + f", prefix length swept t = 1..{cfg.t}", "B": cfg.B,
+                   "k": cfg.k, "H": cfg.H, "D": cfg.D, "S": cfg.S, "V": cfg.V, "n": cfg.n,
+                   "kv_sets_rotated": R},
+        "cross_attn_us_median": round(ca, 3),
+        "roofline": {"bound": "hbm", "kernel": "fs_beam_cross_attn", "achieved": round(ca_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(ca_gbps / HBM_PEAK_GBPS, 4),
+                     "algorithmic_bytes_per_launch": b_ca, "traffic": None},
+        "sweep": rows,
+        "cpu_baseline": None,
+    }
     print(json.dumps(line), flush=True)
     return 0
 
