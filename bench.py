@@ -32,6 +32,10 @@ ROOT = pathlib.Path(__file__).resolve().parent
 sys.path.insert(0, str(ROOT))
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+# The oracle is timed over repeated whole steps until about this much host
+# time is spent (or this many repetitions), and the median is reported.
+ORACLE_BUDGET_S = 10.0
+ORACLE_MAX_REPS = 2000
 
 
 def log(msg: str) -> None:
@@ -528,7 +532,7 @@ def bench_prefix(args, cfg, dev) -> int:
             ref = oracle.prefix_attn(qd, Kpd, Vpd, lens, Ktd, Vtd, t)
             times.append(time.perf_counter() - c0)
             if (args.cpu_reps and len(times) >= args.cpu_reps) or \
-                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                    (not args.cpu_reps and (sum(times) > ORACLE_BUDGET_S or len(times) >= ORACLE_MAX_REPS)):
                 break
         sec = float(np.median(times))
         err = float(np.max(np.abs(out0 - ref)))
@@ -666,7 +670,7 @@ def bench_indirect(args, cfg, dev) -> int:
                                               am["anc"], t)
             times.append(time.perf_counter() - c0)
             if (args.cpu_reps and len(times) >= args.cpu_reps) or \
-                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                    (not args.cpu_reps and (sum(times) > ORACLE_BUDGET_S or len(times) >= ORACLE_MAX_REPS)):
                 break
         sec = float(np.median(times))
         err = float(np.max(np.abs(out0 - ref)))
@@ -774,7 +778,7 @@ def bench_select(args, cfg, dev) -> int:
             ref = oracle.beam_select(d["logits"], d["beam_scores"], d["tokens"], cfg.t, cfg.n, k, c)
             times.append(time.perf_counter() - c0)
             if (args.cpu_reps and len(times) >= args.cpu_reps) or \
-                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                    (not args.cpu_reps and (sum(times) > ORACLE_BUDGET_S or len(times) >= ORACLE_MAX_REPS)):
                 break
         sec = float(np.median(times))
         same = bool(np.array_equal(first[1], ref[1]) and np.array_equal(first[2], ref[2]))
@@ -896,7 +900,7 @@ def bench_reorder(args, cfg, dev) -> int:
             rv = oracle.cache_reorder(vh, par, k, t)
             times.append(time.perf_counter() - c0)
             if (args.cpu_reps and len(times) >= args.cpu_reps) or \
-                    (not args.cpu_reps and (sum(times) > 10.0 or len(times) >= 50)):
+                    (not args.cpu_reps and (sum(times) > ORACLE_BUDGET_S or len(times) >= ORACLE_MAX_REPS)):
                 break
         sec = float(np.median(times))
         api.cache_reorder(Kc, Vc, parent, k, t)
@@ -945,7 +949,7 @@ def cpu_baseline(cfg, base, g, out0, logits0, step_bytes, reps):
         times.append(t2 - t0)
         t_attn.append(t1 - t0)
         t_ng.append(t2 - t1)
-        if (reps and len(times) >= reps) or (not reps and (sum(times) > 10.0 or len(times) >= 50)):
+        if (reps and len(times) >= reps) or (not reps and (sum(times) > ORACLE_BUDGET_S or len(times) >= ORACLE_MAX_REPS)):
             break
     sec = float(np.median(times))
     # One more pass on a single thread, for the per-core figure.
