@@ -37,6 +37,14 @@
  *     in fs_last_error().
  *   - Calls are re-entrant; calls on different streams may run concurrently
  *     as long as they do not share an output or workspace buffer.
+ *   - Graph capture: fs_ngram_block, fs_cache_reorder, fs_beam_ancestry_step
+ *     and the attention calls that take one workgroup per row (128 or more
+ *     (source, head) rows) keep no state between calls and may be captured
+ *     into a HIP graph and replayed.  Calls whose workgroups exchange tagged
+ *     records through the workspace (the attention's split-KV form for
+ *     fewer rows, and fs_beam_select) tell their own records apart by a tag
+ *     passed at launch, which a graph would freeze; they return
+ *     FS_ERR_UNSUPPORTED when `stream` is capturing, before any launch.
  *   - Debug mode: with the environment variable FS_VALIDATE=1 set when the
  *     library is first used, fs_beam_cross_attn copies src_len to the host
  *     (synchronising `stream`) and returns FS_ERR_INVALID_ARG if a length

@@ -66,6 +66,23 @@ unsigned long long next_epoch() {
 
 bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
 
+// A call whose kernels exchange tagged records through the workspace tells
+// its own records from older ones by a tag passed at launch.  Under stream
+// capture that tag would be frozen into the graph, and a replay could take
+// the previous replay's records for its own: such calls are refused there.
+bool capturing(hipStream_t s) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(s, &st) == hipSuccess && st != hipStreamCaptureStatusNone;
+}
+
+// Whether an attention call of n_bh rows over S keys (plus a generated-token
+// job) takes the decomposition that exchanges records.
+bool attn_uses_records(int n_bh, int S, int D, int esize, bool gen_job) {
+    const int C = fs::cross_attn_chunk_keys(D, esize);
+    const int NC = std::max(1, (S + C - 1) / C);
+    return fs::choose_attn_path(n_bh, NC + (gen_job ? 1 : 0)) == fs::AttnPath::kSplit;
+}
+
 // Host-side shape checks shared by the workspace query and the launch.
 // Returns FS_OK or an error status with g_last_error set.
 int check_attn_sizes(int B, int k, int H, int S, int D, int dtype) {
@@ -155,6 +172,9 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
         return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (attn_uses_records(B * H, S, D, (int)esize, false) && capturing(s))
+        return fail(FS_ERR_UNSUPPORTED, "fs_beam_cross_attn: %d rows take the split-KV form, whose tagged records "
+                    "cannot be captured into a graph", B * H);
     if (validate_mode()) {
         std::vector<int32_t> lens((size_t)B);
         hipError_t e = hipMemcpyAsync(lens.data(), src_len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
@@ -227,6 +247,9 @@ int prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *pr
         return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
 
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (attn_uses_records(B * H, N, D, dtype == FS_BF16 ? 2 : 4, t > 0) && capturing(s))
+        return fail(FS_ERR_UNSUPPORTED, "%d rows take the split-KV form, whose tagged records cannot be captured "
+                    "into a graph", B * H);
     if (validate_mode()) {
         std::vector<int32_t> lens((size_t)B);
         hipError_t e = hipMemcpyAsync(lens.data(), prefix_len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
@@ -386,6 +409,9 @@ int fs_beam_select(const float *logits, const float *beam_scores, const int32_t 
         overlaps(workspace, need, tokens, tok_bytes) || overlaps(workspace, need, out_scores, o_bytes) ||
         overlaps(workspace, need, out_beam, o_bytes) || overlaps(workspace, need, out_token, o_bytes))
         return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
+    if (capturing(static_cast<hipStream_t>(stream)))
+        return fail(FS_ERR_UNSUPPORTED, "fs_beam_select exchanges tagged records between its workgroups; it "
+                    "cannot be captured into a graph");
     hipError_t e = fs::launch_beam_select(logits, beam_scores, need_tokens ? tokens : nullptr, ld_tokens, t,
                                           need_tokens ? n : 0, out_scores, out_beam, out_token, B, k, V, c,
                                           static_cast<unsigned long long *>(workspace), next_epoch(),

@@ -1,0 +1,129 @@
+"""The decode step under HIP graph capture.
+
+The cross-attention with one workgroup per row and the n-gram step keep no
+state between calls, so a captured step replays like an eager one: each
+replay, on inputs changed in place between replays (with eager work and
+synchronisations in between), must give the eager call's bits.  Calls whose
+workgroups exchange tagged records (the split-KV attention, the selection
+step) are refused under capture with FS_ERR_UNSUPPORTED, before any launch.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2106_04718_amd import api, workloads
+
+from _gpu import bits, device, say
+
+pytestmark = pytest.mark.gpu
+
+
+def draw(rng, shape):
+    return torch.from_numpy(workloads.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32)).view(np.int16))
+
+
+def fill_inputs(rng, bufs, S, V):
+    """New values in place (host-drawn, copied in), the way a decoder
+    refreshes its buffers between steps."""
+    q, K, Vv, lens, tokens, logits = bufs
+    q.copy_(draw(rng, tuple(q.shape)).view(torch.bfloat16))
+    K.copy_(draw(rng, tuple(K.shape)).view(torch.bfloat16))
+    Vv.copy_(draw(rng, tuple(Vv.shape)).view(torch.bfloat16))
+    lens.copy_(torch.from_numpy(rng.integers(0, S + 1, size=lens.shape[0]).astype(np.int32)))
+    tk = rng.integers(0, 40, size=tuple(tokens.shape)).astype(np.int32)
+    tokens.copy_(torch.from_numpy(tk))
+    logits.copy_(torch.from_numpy(rng.standard_normal(tuple(logits.shape)).astype(np.float32)))
+
+
+def test_captured_step_replays_like_eager_calls():
+    dev = device()
+    B, k, H, S, D, Vsz, t, n = 8, 4, 16, 700, 64, 3000, 60, 3   # 128 rows: one workgroup per row
+    rng = np.random.default_rng(17)
+    q = torch.empty((B, k, H, D), dtype=torch.bfloat16, device=dev)
+    K = torch.empty((B, H, S, D), dtype=torch.bfloat16, device=dev)
+    Vv = torch.empty_like(K)
+    lens = torch.empty((B,), dtype=torch.int32, device=dev)
+    tokens = torch.empty((B * k, t), dtype=torch.int32, device=dev)
+    logits = torch.empty((B * k, Vsz), dtype=torch.float32, device=dev)
+    bufs = (q, K, Vv, lens, tokens, logits)
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_cross_attn_workspace_bytes(B, k, H, S, D, torch.bfloat16), dev)
+    fill_inputs(rng, bufs, S, Vsz)
+    torch.cuda.synchronize()
+
+    def step():
+        api.beam_cross_attn(q, K, Vv, lens, out=out, workspace=ws)
+        api.ngram_block(tokens, n, logits)
+
+    # warm the kernels on a side stream before capture, as torch asks
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+
+    g = torch.cuda.CUDAGraph()
+    say("[graph] capture cross-attention + n-gram")
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+
+    for rep in range(4):
+        say(f"[graph] replay {rep}")
+        fill_inputs(rng, bufs, S, Vsz)
+        logits0 = logits.clone()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got_out, got_logits = bits(out).copy(), bits(logits).copy()
+        # the same inputs, eager, into fresh outputs
+        logits.copy_(logits0)
+        ref_out = api.beam_cross_attn(q, K, Vv, lens, workspace=ws)
+        api.ngram_block(tokens, n, logits)
+        torch.cuda.synchronize()
+        assert np.array_equal(got_out, bits(ref_out)), f"attention, replay {rep}"
+        assert np.array_equal(got_logits, bits(logits)), f"n-gram, replay {rep}"
+
+
+def test_record_exchanging_calls_are_refused_under_capture():
+    dev = device()
+    rng = np.random.default_rng(5)
+    # 2 rows: the split-KV form, which keeps tagged records in the workspace
+    B, k, H, S, D = 2, 4, 1, 600, 64
+    q = draw(rng, (B, k, H, D)).view(torch.bfloat16).to(dev)
+    K = draw(rng, (B, H, S, D)).view(torch.bfloat16).to(dev)
+    Vv = draw(rng, (B, H, S, D)).view(torch.bfloat16).to(dev)
+    lens = torch.tensor([600, 300], dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_cross_attn_workspace_bytes(B, k, H, S, D, torch.bfloat16), dev)
+    logits = torch.from_numpy(rng.standard_normal((B * k, 500)).astype(np.float32)).to(dev)
+    scores = torch.zeros(B * k, dtype=torch.float32, device=dev)
+    sel_out = (torch.empty((B, 8), dtype=torch.float32, device=dev), torch.empty((B, 8), dtype=torch.int32, device=dev),
+               torch.empty((B, 8), dtype=torch.int32, device=dev))
+    sel_ws = api.new_workspace(api.beam_select_workspace_bytes(B, k, 500, 8), dev)
+    tok = torch.zeros((B * k, 4), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say("[graph] refused calls under capture")
+    errors = []
+    with torch.cuda.graph(g):
+        api.ngram_block(tok, 3, logits)   # something capturable, so the graph is not empty
+        try:
+            api.beam_cross_attn(q, K, Vv, lens, out=out, workspace=ws)
+        except Exception as e:   # noqa: BLE001 - the library's error type
+            errors.append(str(e))
+        try:
+            api.beam_select(logits, scores, k, 8, out=sel_out, workspace=sel_ws)
+        except Exception as e:   # noqa: BLE001
+            errors.append(str(e))
+    torch.cuda.synchronize()
+    assert len(errors) == 2, errors
+    assert "captured" in errors[0] and "captured" in errors[1], errors
+    g.replay()
+    torch.cuda.synchronize()
+    # outside capture the same calls run
+    api.beam_cross_attn(q, K, Vv, lens, out=out, workspace=ws)
+    api.beam_select(logits, scores, k, 8, out=sel_out, workspace=sel_ws)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()
