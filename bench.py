@@ -917,12 +917,14 @@ def bench_reorder(args, cfg, dev) -> int:
 
 
 def kernel_source_sha() -> str:
-    """Hash of what the kernels are built from: the sources and the build
-    flags (a stored traffic figure is only used while it matches)."""
+    """Hash of what the kernels and their launches are built from: the HIP
+    sources, the launch declarations and the build flags (a stored traffic
+    figure is only used while it matches; host-side argument checks do not
+    enter it)."""
     import hashlib
     h = hashlib.sha256()
     pkg = ROOT / "paper_2106_04718_amd"
-    for p in [*sorted((pkg / "csrc").glob("*")), pkg / "build.py"]:
+    for p in [*sorted((pkg / "csrc").glob("*.hip")), pkg / "csrc" / "launch.h", pkg / "build.py"]:
         h.update(p.read_bytes())
     return h.hexdigest()[:16]
 
