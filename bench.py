@@ -118,6 +118,39 @@ def launch_spread(stream, fn, K: int, parts: int = 10) -> dict:
             "p90": round(float(np.percentile(us, 90)), 3), "subregions": parts, "calls_each": per}
 
 
+def graph_step_us(dev, step, n_steps: int, replays: int = 10):
+    """Per-step time when n_steps steps (the K/V rotation included) are
+    captured into one HIP graph and the graph is replayed: the same kernels
+    without the host's launch calls between them.  None if a call refuses
+    capture."""
+    import torch
+    try:
+        cur = torch.cuda.current_stream(dev)
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(cur)
+        with torch.cuda.stream(side):
+            for i in range(n_steps):
+                step(i)
+        cur.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for i in range(n_steps):
+                step(i)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cur)
+        for _ in range(replays):
+            g.replay()
+        b.record(cur)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / (replays * n_steps)
+    except Exception:  # noqa: BLE001 - a decomposition that cannot be captured
+        return None
+
+
 def load_traffic(path: str, name: str):
     """HBM bytes per launch from the counter summary, if it was taken on the
     current kernel sources."""
@@ -274,6 +307,7 @@ def main() -> int:
     ng_us = max(float(np.median([a - b for a, b in pairs])), 0.0)
     step_spread = launch_spread(stream, step, K_)
     ca_spread = launch_spread(stream, ca_only, K_)
+    g_us = graph_step_us(dev, step, 3 * R)
     ms_per_step = step_us * 1e-3
     b_ca = attn_bytes(cfg, lens)
     b_ng = ngram_bytes(cfg.rows, cfg.t, bans)
@@ -285,6 +319,8 @@ def main() -> int:
         f"= {ca_gbps:.0f} GB/s ({100 * ca_gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
         f"{100 * ca_gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s); "
         f"n-gram {ng_us:.2f} us = {100 * ng_us / (ca_us + ng_us):.1f}% of the step")
+    if g_us is not None:
+        log(f"the same step replayed from a HIP graph of {3 * R} steps: {g_us:.2f} us per step")
 
     traffic = load_traffic(args.traffic, cfg.name)
 
@@ -310,6 +346,7 @@ def main() -> int:
         "cross_attn_us_spread": ca_spread,
         "ngram_us": round(ng_us, 3),
         "ngram_share_of_step": round(ng_us / (ca_us + ng_us), 4),
+        "step_us_graph": None if g_us is None else round(g_us, 3),
         "timing_rounds": max(1, args.rounds),
         "copy_gbps": round(copy_gbps, 1),
         "roofline": {"bound": "hbm", "kernel": "fs_beam_cross_attn", "achieved": round(ca_gbps, 1),
