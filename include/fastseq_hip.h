@@ -65,7 +65,8 @@ extern "C" {
 typedef enum {
     FS_OK = 0,
     FS_ERR_INVALID_ARG = 1,  /* bad pointer, size, alignment, aliasing or workspace */
-    FS_ERR_UNSUPPORTED = 2,  /* valid but not implemented: D, k or dtype outside the set below */
+    FS_ERR_UNSUPPORTED = 2,  /* valid but not implemented: D, k or dtype outside the set below,
+                                or a record-exchanging call under stream capture */
     FS_ERR_HIP = 3           /* a HIP runtime call or kernel launch failed */
 } fs_status_t;
 
@@ -131,8 +132,9 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  * negative sizes, a pointer of q/K/V/out/workspace not 16-byte aligned, a
  * workspace that is too small, or out or the workspace overlapping another
  * argument; sizes too large for one launch;
- * FS_ERR_UNSUPPORTED for D, k or dtype outside the set above; FS_ERR_HIP for
- * a failed launch.  B == 0, k == 0 or H == 0 returns FS_OK with no launch.
+ * FS_ERR_UNSUPPORTED for D, k or dtype outside the set above, or for the
+ * split-KV form (fewer than 128 rows) while `stream` is capturing; FS_ERR_HIP
+ * for a failed launch.  B == 0, k == 0 or H == 0 returns FS_OK with no launch.
  */
 int fs_beam_cross_attn(const void *q, const void *K, const void *V,
                        const int32_t *src_len, void *out,
@@ -255,7 +257,8 @@ size_t fs_beam_select_workspace_bytes(int B, int k, int V, int c);
  * sizes, n < 0, ld_tokens < t with n > 0, c > k*V, pointers not 4-byte
  * aligned, a workspace that is too small, or an output overlapping an input
  * or another output; FS_ERR_UNSUPPORTED for c, k or the candidate count
- * outside the set above; FS_ERR_HIP for a failed launch.  B == 0 returns
+ * outside the set above, or while `stream` is capturing; FS_ERR_HIP for a
+ * failed launch.  B == 0 returns
  * FS_OK with no launch.  If a partial record is not seen within about 10 ms
  * (which does not happen in a working launch), the source's outputs are NaN
  * and -1.
