@@ -1,9 +1,12 @@
 #!/usr/bin/env python3
 """Benchmark of the beam-search decode step on one MI355X.
 
-One step = the whole hot path on one batch: fs_beam_cross_attn (the k beams
-of every source read its one de-duplicated K/V copy) followed by
-fs_ngram_block on the step's logits, back to back on one stream.  Inputs are
+One step = the whole hot path on one batch, in one launch
+(fs_beam_decode_step): the cross-attention in which the k beams of every
+source read its one de-duplicated K/V copy, with the no-repeat-n-gram scan of
+the step's hypotheses done by extra workgroups of the same grid.  The same
+step as two launches (fs_beam_cross_attn, then fs_ngram_block) is timed
+beside it.  Inputs are
 seeded synthetic BART-large-shaped tensors (workloads.py), resident in HBM
 before timing starts.  Each step reads a different K/V set, rotating over at
 least 1 GiB of sets so that the 256 MB last-level cache cannot hold them.
@@ -64,6 +67,9 @@ def parse():
     ap.add_argument("--copy-calibrate", type=float, default=0.0, metavar="GIB",
                     help="instead of the step, run a plain device copy of this many GiB "
                          "(reference for the FETCH_SIZE/WRITE_SIZE counters)")
+    ap.add_argument("--summarize-trace", default="", metavar="CSV",
+                    help="instead of running, print the kernel durations of a rocprofv3 kernel-trace CSV "
+                         "grouped by kernel and grid size (a fused step and the attention alone differ in grid)")
     ap.add_argument("--traffic", default=str(ROOT / "profiles" / "traffic.json"),
                     help="HBM traffic per launch measured with rocprofv3 counters")
     return ap.parse_args()
@@ -95,14 +101,37 @@ def prefix_bytes(cfg, lens, t: int) -> int:
     return kv + gen + qo + 4 * cfg.B
 
 
+SETTLE_MS = 20.0        # back-to-back steps before the warm-up, so that the clocks are up
+SPREAD_MIN_CALLS = 20   # calls per sub-region of the spread, whatever --steps is
+
+
+def settle(stream, fn, ms: float = SETTLE_MS) -> int:
+    """Run ``fn(i)`` back to back for about ``ms`` of GPU time (untimed);
+    returns the number of calls."""
+    import torch
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    calls, batch = 0, 50
+    torch.cuda.synchronize()
+    a.record(stream)
+    while True:
+        for i in range(batch):
+            fn(calls + i)
+        calls += batch
+        b.record(stream)
+        b.synchronize()
+        if a.elapsed_time(b) >= ms or calls >= 100000:
+            return calls
+
+
 def launch_spread(stream, fn, K: int, parts: int = 10) -> dict:
     """Median, p10 and p90 of the mean per-call time of ``fn(i)`` over
-    ``parts`` equal sub-regions of K back-to-back calls (events only at the
-    sub-region ends).  Timed in a pass of its own, so that its extra events
-    never enter the headline means."""
+    ``parts`` equal sub-regions of back-to-back calls (events only at the
+    sub-region ends), each of at least SPREAD_MIN_CALLS calls.  Timed in a
+    pass of its own, so that its extra events never enter the headline
+    means."""
     import numpy as np
     import torch
-    per = max(1, K // parts)
+    per = max(SPREAD_MIN_CALLS, K // parts)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(parts + 1)]
     torch.cuda.synchronize()
     i = 0
@@ -197,8 +226,29 @@ def copy_calibrate(gib: float) -> None:
     print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
 
 
+def summarize_trace(path: str) -> int:
+    """Kernel durations of a rocprofv3 --kernel-trace CSV, grouped by
+    (kernel, workgroups): device begin/end timestamps, in microseconds."""
+    import csv
+    import statistics
+    groups: dict = {}
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            wg = int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"]))
+            us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3
+            groups.setdefault((r["Kernel_Name"], wg, int(r["Workgroup_Size_X"])), []).append(us)
+    print(f"{'kernel':70s} {'workgroups':>10s} {'threads':>7s} {'calls':>6s} {'avg us':>8s} "
+          f"{'median':>8s} {'min us':>8s} {'max us':>8s}")
+    for (name, wg, th), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        print(f"{name[:70]:70s} {wg:10d} {th:7d} {len(v):6d} {statistics.fmean(v):8.2f} "
+              f"{statistics.median(v):8.2f} {min(v):8.2f} {max(v):8.2f}")
+    return 0
+
+
 def main() -> int:
     args = parse()
+    if args.summarize_trace:
+        return summarize_trace(args.summarize_trace)
     if args.gpus != 1:
         print(f"bench.py: the benchmark runs on one GPU; --gpus {args.gpus} is not supported "
               "(the decode step would shard by source with no exchange between GPUs)",
@@ -261,33 +311,41 @@ def main() -> int:
         f"{time.perf_counter() - t0:.1f}s")
 
     def step(i: int):
+        # the whole step in one launch: the n-gram rows ride in the attention grid
+        api.beam_decode_step(q, Ks[i % R], Vs[i % R], lens_d, tokens_d, cfg.n, logits_d, out=out, workspace=ws)
+
+    def step_separate(i: int):
         api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
         api.ngram_block(tokens_d, cfg.n, logits_d)
 
+    def ca_only(i: int):
+        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
+
     # ---- first step: outputs kept for the CPU-baseline comparison ---------
-    api.beam_cross_attn(q, Ks[0], Vs[0], lens_d, out=out, workspace=ws)
-    api.ngram_block(tokens_d, cfg.n, logits_d)
+    step(0)
     torch.cuda.synchronize()
     out0 = out.float().cpu().numpy().astype(np.float64)
     logits0 = logits_d.cpu().numpy()
     bans = int(np.isneginf(logits0).sum())
 
-    # ---- warm-up and timed regions -----------------------------------------
-    # Region A times exactly K steps with events only at its two ends: event
-    # records between kernels would themselves add several microseconds per
-    # step.  It gives the headline step time.  Then `rounds` pairs of
-    # regions alternate: K steps (A_r) and K back-to-back cross-attention
-    # launches on the same stream with the same K/V rotation (B_r).  The
-    # kernel's average duration is the median of B_r; the n-gram step's cost
-    # is the median of A_r - B_r (pairing cancels slow clock drift).
+    # ---- settle, warm-up and timed regions ---------------------------------
+    # The clocks are settled first by SETTLE_MS of back-to-back steps, so
+    # that a short warm-up (--warmup) still times a GPU at its working
+    # clocks; then W warm-up steps and region A, which times exactly K steps
+    # with events only at its two ends (event records between kernels would
+    # themselves add microseconds per step).  Region A gives the headline.
+    # Then `rounds` triples of regions alternate on the same stream with the
+    # same K/V rotation: K steps (A_r), K cross-attention launches alone
+    # (B_r) and K steps as two launches (C_r).  The cross-attention's average
+    # launch duration is the median of B_r; the n-gram scan's cost in the
+    # fused step is the median of A_r - B_r (pairing cancels clock drift),
+    # and in the two-launch step the median of C_r - B_r.
+    stream = torch.cuda.current_stream(dev)
+    settle_calls = settle(stream, step)
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     K_ = args.steps
-    stream = torch.cuda.current_stream(dev)
-
-    def ca_only(i: int):
-        api.beam_cross_attn(q, Ks[i % R], Vs[i % R], lens_d, out=out, workspace=ws)
 
     def region_us(fn) -> float:
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -302,9 +360,11 @@ def main() -> int:
     w0 = time.perf_counter()
     step_us = region_us(step)
     wall = time.perf_counter() - w0
-    pairs = [(region_us(step), region_us(ca_only)) for _ in range(max(1, args.rounds))]
-    ca_us = float(np.median([b for _, b in pairs]))
-    ng_us = max(float(np.median([a - b for a, b in pairs])), 0.0)
+    trips = [(region_us(step), region_us(ca_only), region_us(step_separate)) for _ in range(max(1, args.rounds))]
+    ca_us = float(np.median([b for _, b, _ in trips]))
+    ng_us = max(float(np.median([a - b for a, b, _ in trips])), 0.0)
+    sep_us = float(np.median([c for _, _, c in trips]))
+    ng_sep_us = max(float(np.median([c - b for _, b, c in trips])), 0.0)
     step_spread = launch_spread(stream, step, K_)
     ca_spread = launch_spread(stream, ca_only, K_)
     g_us = graph_step_us(dev, step, 3 * R)
@@ -315,10 +375,11 @@ def main() -> int:
     value = b_step / (ms_per_step * 1e-3) / 1e9
     ca_gbps = b_ca / (ca_us * 1e-6) / 1e9
     copy_gbps = copy_bandwidth(dev)
-    log(f"step {step_us:.2f} us (wall {wall / K_ * 1e6:.2f} us) = {value:.0f} GB/s; cross-attn {ca_us:.2f} us "
-        f"= {ca_gbps:.0f} GB/s ({100 * ca_gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
+    log(f"step {step_us:.2f} us (one launch; wall {wall / K_ * 1e6:.2f} us) = {value:.0f} GB/s; cross-attn "
+        f"{ca_us:.2f} us = {ca_gbps:.0f} GB/s ({100 * ca_gbps / HBM_PEAK_GBPS:.1f}% of 8 TB/s, "
         f"{100 * ca_gbps / copy_gbps:.1f}% of the measured copy bandwidth {copy_gbps:.0f} GB/s); "
-        f"n-gram {ng_us:.2f} us = {100 * ng_us / (ca_us + ng_us):.1f}% of the step")
+        f"n-gram adds {ng_us:.2f} us = {100 * ng_us / step_us:.1f}% of the step; as two launches the step takes "
+        f"{sep_us:.2f} us (n-gram {100 * ng_sep_us / sep_us:.1f}%)")
     if g_us is not None:
         log(f"the same step replayed from a HIP graph of {3 * R} steps: {g_us:.2f} us per step")
 
@@ -342,10 +403,14 @@ def main() -> int:
                    "S": cfg.S, "t": cfg.t, "V": cfg.V, "n": cfg.n, "kv_sets_rotated": R,
                    "bytes_per_step": b_step},
         "step_us_spread": step_spread,
+        "step_launches": 1,
+        "settle_calls": settle_calls,
         "cross_attn_us": round(ca_us, 3),
         "cross_attn_us_spread": ca_spread,
         "ngram_us": round(ng_us, 3),
-        "ngram_share_of_step": round(ng_us / (ca_us + ng_us), 4),
+        "ngram_share_of_step": round(ng_us / step_us, 4),
+        "step_two_launches_us": round(sep_us, 3),
+        "ngram_share_two_launches": round(ng_sep_us / sep_us, 4),
         "step_us_graph": None if g_us is None else round(g_us, 3),
         "timing_rounds": max(1, args.rounds),
         "copy_gbps": round(copy_gbps, 1),
@@ -430,8 +495,7 @@ def bench_sweep(args, cfg, dev) -> int:
         bans = int(torch.isneginf(logits_d).sum().item())
 
         def step(i: int, tok_t=tok_t):
-            ca_only(i)
-            api.ngram_block(tok_t, cfg.n, logits_d)
+            api.beam_decode_step(q, Ks[i % R], Vs[i % R], lens_d, tok_t, cfg.n, logits_d, out=out, workspace=ws)
 
         a_us, b_us = region_us(step), region_us(ca_only)
         b_step = b_ca + ngram_bytes(cfg.rows, t, bans)

@@ -10,6 +10,9 @@
  *   fs_ngram_block      no-repeat-n-gram blocking on the GPU (Section 4.2,
  *                       Algorithm 1): logits of tokens that would repeat an
  *                       earlier n-gram become -inf, in place.
+ *   fs_beam_decode_step both of the above in one launch: the decode step's
+ *                       cross-attention with its n-gram rows scanned by extra
+ *                       workgroups of the same grid.
  *   fs_beam_prefix_attn self-attention over a split cache: the prefix shared
  *                       by a sample's beams is stored once (Section 4.1.1;
  *                       Appendix A, Eq. 2-3).
@@ -46,9 +49,11 @@
  *     passed at launch, which a graph would freeze; they return
  *     FS_ERR_UNSUPPORTED when `stream` is capturing, before any launch.
  *   - Debug mode: with the environment variable FS_VALIDATE=1 set when the
- *     library is first used, fs_beam_cross_attn copies src_len to the host
- *     (synchronising `stream`) and returns FS_ERR_INVALID_ARG if a length
- *     lies outside [0, S] instead of clamping it.
+ *     library is first used (or after fs_set_tuning(FS_TUNE_VALIDATE, 1)),
+ *     the attention calls copy src_len / prefix_len
+ *     to the host (synchronising `stream`) and return FS_ERR_INVALID_ARG if
+ *     a length lies outside [0, S] instead of clamping it; on a capturing
+ *     stream, where that copy cannot run, they return FS_ERR_UNSUPPORTED.
  */
 #ifndef FASTSEQ_HIP_H
 #define FASTSEQ_HIP_H
@@ -124,8 +129,10 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  *            run concurrently.
  *   stream   hipStream_t (NULL = default stream)
  * Supported: dtype FS_F32 or FS_BF16, D in {16, 32, 64, 128}, 1 <= k <= 8,
- * B, H, S >= 0 with B*k*H below 2^31 and a launch grid of about
- * B*H*S*D*esize/8192 workgroups (esize = 2 or 4 bytes) below 2^31.
+ * B, H, S >= 0 with B*k*H below 2^31, a launch grid of about
+ * B*H*S*D*esize/8192 workgroups (esize = 2 or 4 bytes) below 2^31, and one
+ * (source, head) block of S*D*esize bytes below 2 GiB (0x7ff00000 bytes;
+ * FS_ERR_UNSUPPORTED above).
  * Arithmetic: products and sums in fp32; the result does not depend on k,
  * B or the beam's position (bitwise), only on (L, S, D, dtype) and the data.
  * Errors: FS_ERR_INVALID_ARG for a null pointer with non-empty sizes,
@@ -176,7 +183,8 @@ size_t fs_beam_prefix_attn_workspace_bytes(int B, int k, int H, int N, int T, in
  *                               (the rules of fs_beam_cross_attn's workspace)
  * Supported sizes, dtypes, arithmetic, determinism and errors are those of
  * fs_beam_cross_attn (with N in the role of S); in addition t > T or a
- * negative T or t is FS_ERR_INVALID_ARG.  The result bits do not depend on k,
+ * negative T or t is FS_ERR_INVALID_ARG, and a (hypothesis, head) block of
+ * T*D*esize bytes above 0x7ff00000 is FS_ERR_UNSUPPORTED.  The result bits do not depend on k,
  * B or the beam's position, nor on whether the prefix is shared or passed
  * replicated per beam.
  */
@@ -208,6 +216,58 @@ int fs_beam_prefix_attn(const void *q, const void *Kp, const void *Vp, const int
  */
 int fs_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t, int n,
                    float *logits, int V, void *stream);
+
+/*
+ * One decode step of beam search in one launch: fs_beam_cross_attn followed
+ * by fs_ngram_block on the step's hypotheses (Appendix B, Eq. 4; Section 4.2,
+ * Algorithm 1).  The B*k rows of the n-gram scan are taken by extra
+ * workgroups at the head of the attention grid, so the scan runs under the
+ * attention's K/V stream instead of after it.  The results are bit for bit
+ * those of the two calls:
+ *     fs_beam_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype,
+ *                        workspace, workspace_bytes, stream);
+ *     fs_ngram_block(tokens, ld_tokens, B*k, t, n, logits, vocab, stream);
+ * Arguments are those of the two calls (vocab is fs_ngram_block's V); the
+ * workspace is fs_beam_cross_attn's.  Besides the errors of both calls,
+ * FS_ERR_INVALID_ARG when logits overlap q, K, V, out, src_len or the
+ * workspace, or tokens overlap out or the workspace.  When one half is
+ * empty (B, k or H == 0; t < n or vocab == 0) only the other runs.
+ */
+int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32_t *src_len, void *out,
+                        int B, int k, int H, int S, int D, int dtype,
+                        const int32_t *tokens, int ld_tokens, int t, int n, float *logits, int vocab,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Tuning controls, for tests and measurements: they replace a size rule of
+ * the library for every later call in the process (every thread).  Results
+ * do not depend on them except where a call's documentation says so (the
+ * slice count of fs_beam_select).  Returns the previous value, or -1 for an
+ * unknown knob or value (nothing changes then).
+ *   FS_TUNE_ATTN_PATH      decomposition of the attention calls:
+ *                          FS_ATTN_PATH_AUTO (the size rule), _SPLIT (one
+ *                          workgroup per chunk of 256 keys at D = 64 bf16, with
+ *                          partial records), _WHOLE1/_WHOLE2/_WHOLE4 (one
+ *                          workgroup of 4/8/16 waves per (source, head)).
+ *                          Every decomposition gives the same bits.
+ *   FS_TUNE_SELECT_SLICES  vocabulary slices per row of fs_beam_select
+ *                          (0: the size rule), within that call's limits.
+ *   FS_TUNE_VALIDATE       debug mode on (1) or off (0); it starts as the
+ *                          environment variable FS_VALIDATE sets it.
+ */
+enum {
+    FS_TUNE_ATTN_PATH = 1,
+    FS_TUNE_SELECT_SLICES = 2,
+    FS_TUNE_VALIDATE = 3
+};
+enum {
+    FS_ATTN_PATH_AUTO = 0,
+    FS_ATTN_PATH_SPLIT = 1,
+    FS_ATTN_PATH_WHOLE1 = 2,
+    FS_ATTN_PATH_WHOLE2 = 3,
+    FS_ATTN_PATH_WHOLE4 = 4
+};
+int fs_set_tuning(int knob, int value);
 
 /*
  * Workspace, in bytes, that fs_beam_select needs for these sizes (per
@@ -249,7 +309,7 @@ size_t fs_beam_select_workspace_bytes(int B, int k, int V, int c);
  * words (k * slices * (2 + 2c)); the slice count is reduced to fit these
  * when it can be, so only a vocabulary above 16381 * (1024 / (k * c))
  * logits can exceed them.  The slice count follows from the sizes;
- * FS_SELECT_SLICES (read once per process) sets it within the same limits.
+ * fs_set_tuning(FS_TUNE_SELECT_SLICES, n) sets it within the same limits.
  * Arithmetic: fp32 (the normaliser from per-slice maxima and sums of exp);
  * the order and the bits of the result depend on the data, the slice count
  * and the address of logits modulo 16 bytes, never on run or launch.

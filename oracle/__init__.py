@@ -9,10 +9,13 @@ module only marshals numpy arrays into it:
 
 * :func:`cross_attn` -- masked softmax(q K^T / sqrt(D)) V with one K/V copy
   per source shared by its k beams (Appendix B, Eq. 4).
+* :func:`cross_attn_replicated` -- the same over K/V replicated per beam,
+  [B*k,H,S,D] (the layout of Eq. 1 that Eq. 4 replaces).
 * :func:`prefix_attn` -- self-attention over a shared prefix cache plus a
   per-beam generated-token cache, one softmax over both (Appendix A, Eq. 3).
 * :func:`ngram_block` -- no-repeat-n-gram blocking as its definition
   (Section 4.2, Algorithm 1): ban v iff (last n-1 tokens, v) already occurred.
+* :func:`ngram_banned` -- the same bans as a sorted (row, token) list.
 * :func:`beam_select` -- one beam-search selection step (Section 2.1): the c
   best (running score + log-probability) candidates of each source, with the
   n-gram bans applied to the log-probabilities.
@@ -50,6 +53,10 @@ def _lib():
         lib = ctypes.CDLL(str(path))
         lib.oracle_cross_attn.argtypes = [_dp, _dp, _dp, _ip, _dp] + [ctypes.c_int] * 5
         lib.oracle_cross_attn.restype = ctypes.c_int
+        lib.oracle_cross_attn_replicated.argtypes = [_dp, _dp, _dp, _ip, _dp] + [ctypes.c_int] * 5
+        lib.oracle_cross_attn_replicated.restype = ctypes.c_int
+        lib.oracle_ngram_banned.argtypes = [_ip] + [ctypes.c_int] * 5 + [_ip, ctypes.c_long]
+        lib.oracle_ngram_banned.restype = ctypes.c_long
         lib.oracle_prefix_attn.argtypes = [_dp, _dp, _dp, _ip, _dp, _dp, ctypes.c_int, _dp] + [ctypes.c_int] * 6
         lib.oracle_prefix_attn.restype = ctypes.c_int
         lib.oracle_ngram_block.argtypes = [_ip, ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -123,6 +130,32 @@ def cross_attn_f64(q, K, V, src_len) -> np.ndarray:
     return out
 
 
+def cross_attn_replicated(q, K, V, src_len) -> np.ndarray:
+    """fp64 attention with K/V replicated per beam (the layout of Eq. 1).
+
+    q [B,k,H,D]; K, V [B*k,H,S,D]: hypothesis b*k + i reads K[b*k + i];
+    src_len [B] (the length of each source, shared by its beams).
+    """
+    qd = np.ascontiguousarray(widen(q))
+    Kd = np.ascontiguousarray(widen(K))
+    Vd = np.ascontiguousarray(widen(V))
+    if qd.ndim != 4 or Kd.ndim != 4 or Vd.shape != Kd.shape:
+        raise ValueError("q must be [B,k,H,D] and K, V [B*k,H,S,D]")
+    B, k, H, D = qd.shape
+    if Kd.shape[0] != B * k or Kd.shape[1] != H or Kd.shape[3] != D:
+        raise ValueError(f"shape mismatch q{qd.shape} K{Kd.shape}")
+    lens = np.ascontiguousarray(np.asarray(src_len, dtype=np.int32))
+    if lens.shape != (B,):
+        raise ValueError("src_len must be [B]")
+    out = np.empty((B, k, H, D), dtype=np.float64)
+    rc = _lib().oracle_cross_attn_replicated(
+        qd.ctypes.data_as(_dp), Kd.ctypes.data_as(_dp), Vd.ctypes.data_as(_dp),
+        lens.ctypes.data_as(_ip), out.ctypes.data_as(_dp), B, k, H, Kd.shape[2], D)
+    if rc != 0:
+        raise ValueError("oracle_cross_attn_replicated rejected its arguments")
+    return out
+
+
 def prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, t: int) -> np.ndarray:
     """fp64 self-attention over a split cache (Eq. 2-3).
 
@@ -184,6 +217,30 @@ def ngram_block(tokens, n: int, logits, t: int | None = None) -> np.ndarray:
     if rc != 0:
         raise ValueError("oracle_ngram_block rejected its arguments")
     return lg
+
+
+def ngram_banned(tokens, n: int, V: int, t: int | None = None) -> np.ndarray:
+    """The no-repeat-n-gram bans as an int32 array of (row, token) pairs,
+    sorted by row then token, each once (the positions that
+    :func:`ngram_block` sets to -inf)."""
+    tok = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    if tok.ndim != 2:
+        raise ValueError("tokens must be [rows, ld]")
+    rows, ld = tok.shape
+    if t is None:
+        t = ld
+    lib = _lib()
+    cap = max(1, rows * max(0, int(t) - int(n) + 1))
+    for _ in range(2):
+        pairs = np.empty((cap, 2), dtype=np.int32)
+        got = lib.oracle_ngram_banned(tok.ctypes.data_as(_ip), ld, rows, int(t), int(n), int(V),
+                                      pairs.ctypes.data_as(_ip), cap)
+        if got < 0:
+            raise ValueError("oracle_ngram_banned rejected its arguments")
+        if got <= cap:
+            return pairs[:got].copy()
+        cap = int(got)
+    raise RuntimeError("oracle_ngram_banned: pair count changed between calls")
 
 
 def beam_select(logits, beam_scores, tokens, t: int, n: int, k: int, c: int):

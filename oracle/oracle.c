@@ -16,8 +16,11 @@
  *                       cache (Appendix B, Eq. 4), with a key-length mask.
  *   oracle_prefix_attn  self-attention with a shared prefix cache and a per-beam
  *                       generated-token cache (Appendix A, Eq. 2 and Eq. 3).
+ *   oracle_cross_attn_replicated  the same over K/V replicated per beam (the
+ *                       layout of Eq. 1), the form Eq. 4 replaces.
  *   oracle_ngram_block  no-repeat-n-gram blocking (Section 4.2, Algorithm 1)
  *                       written as its plain definition.
+ *   oracle_ngram_banned the same bans as a sorted list of (row, token) pairs.
  *   oracle_beam_select  one beam-search selection step (Section 2.1) over
  *                       log-probabilities with the n-gram bans applied.
  *   oracle_cache_reorder the per-beam cache reorder that follows a selection
@@ -33,6 +36,50 @@
 #ifdef _OPENMP
 #include <omp.h>
 #endif
+
+/* One (source, beam, head) row of Eq. 4: out = softmax(q K^T / sqrt(D)) V over
+ * the first L rows of Kbh / Vbh ([S, D] each), in fp64.  L == 0 gives 0. */
+static void attend_row(const double *qrow, const double *Kbh, const double *Vbh, int L, int D,
+                       double *orow)
+{
+    if (L <= 0) {
+        for (int d = 0; d < D; ++d) orow[d] = 0.0;
+        return;
+    }
+    const double root_d = sqrt((double)D);
+    double *w = (double *)malloc(sizeof(double) * (size_t)L);
+    if (!w) abort();
+
+    /* scores: s_j = (q . K_j) / sqrt(D) */
+    for (int j = 0; j < L; ++j) {
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d)
+            dot += qrow[d] * Kbh[(size_t)j * D + d];
+        w[j] = dot / root_d;
+    }
+    /* softmax over the valid keys */
+    double m = -INFINITY;
+    for (int j = 0; j < L; ++j)
+        if (w[j] > m) m = w[j];
+    double Z = 0.0;
+    for (int j = 0; j < L; ++j) {
+        w[j] = exp(w[j] - m);
+        Z += w[j];
+    }
+    /* weighted sum of the values */
+    for (int d = 0; d < D; ++d) {
+        double acc = 0.0;
+        for (int j = 0; j < L; ++j)
+            acc += w[j] * Vbh[(size_t)j * D + d];
+        orow[d] = acc / Z;
+    }
+    free(w);
+}
+
+static int clamp_len(int L, int S)
+{
+    return L < 0 ? 0 : (L > S ? S : L);
+}
 
 /*
  * Encoder-decoder attention with de-duplicated K/V (Appendix B, Eq. 4).
@@ -68,7 +115,6 @@ int oracle_cross_attn(const double *q, const double *K, const double *V,
     if (!q || !K || !V || !src_len || !out)
         return 1;
 
-    const double root_d = sqrt((double)D);
     const long rows = (long)B * k * H;
 
 #pragma omp parallel for schedule(dynamic, 4)
@@ -76,46 +122,43 @@ int oracle_cross_attn(const double *q, const double *K, const double *V,
         /* r = (b*k + i)*H + h: source b, beam i, head h */
         const int h = (int)(r % H);
         const int b = (int)(r / ((long)H * k));
-        const double *qrow = q + r * D;  /* q[b, i, h, :] */
-        double *orow = out + r * D;      /* out[b, i, h, :] */
         const double *Kbh = K + ((size_t)b * H + h) * (size_t)S * D;
         const double *Vbh = V + ((size_t)b * H + h) * (size_t)S * D;
+        attend_row(q + r * D, Kbh, Vbh, clamp_len(src_len[b], S), D, out + r * D);
+    }
+    return 0;
+}
 
-        int L = src_len[b];
-        if (L < 0) L = 0;
-        if (L > S) L = S;
-        if (L == 0) {
-            for (int d = 0; d < D; ++d) orow[d] = 0.0;
-            continue;
-        }
+/*
+ * The same attention over the conventional layout of Eq. 1, where the
+ * encoder keys and values are replicated for every beam: K, V [B*k, H, S, D],
+ * hypothesis b*k + i reading its own copy K[b*k + i] (with the length of its
+ * source, src_len[b]).  With every copy of a source equal, Eq. 4 holds that
+ * the result is that of oracle_cross_attn on one copy.
+ * Returns 0, or 1 for invalid sizes (nothing is written then).
+ */
+int oracle_cross_attn_replicated(const double *q, const double *K, const double *V,
+                                 const int32_t *src_len, double *out,
+                                 int B, int k, int H, int S, int D)
+{
+    if (B < 0 || k < 0 || H < 0 || S < 0 || D < 1)
+        return 1;
+    if (B == 0 || k == 0 || H == 0)
+        return 0;
+    if (!q || !K || !V || !src_len || !out)
+        return 1;
 
-        double *w = (double *)malloc(sizeof(double) * (size_t)L);
-        if (!w) abort();
+    const long rows = (long)B * k * H;
 
-        /* scores: s_j = (q . K_j) / sqrt(D) */
-        for (int j = 0; j < L; ++j) {
-            double dot = 0.0;
-            for (int d = 0; d < D; ++d)
-                dot += qrow[d] * Kbh[(size_t)j * D + d];
-            w[j] = dot / root_d;
-        }
-        /* softmax over the valid keys */
-        double m = w[0];
-        for (int j = 1; j < L; ++j)
-            if (w[j] > m) m = w[j];
-        double Z = 0.0;
-        for (int j = 0; j < L; ++j) {
-            w[j] = exp(w[j] - m);
-            Z += w[j];
-        }
-        /* weighted sum of the values */
-        for (int d = 0; d < D; ++d) {
-            double acc = 0.0;
-            for (int j = 0; j < L; ++j)
-                acc += w[j] * Vbh[(size_t)j * D + d];
-            orow[d] = acc / Z;
-        }
-        free(w);
+#pragma omp parallel for schedule(dynamic, 4)
+    for (long r = 0; r < rows; ++r) {
+        /* r = hyp*H + h with hyp = b*k + i */
+        const int h = (int)(r % H);
+        const long hyp = r / H;
+        const int b = (int)(hyp / k);
+        const double *Kbh = K + ((size_t)hyp * H + h) * (size_t)S * D;
+        const double *Vbh = V + ((size_t)hyp * H + h) * (size_t)S * D;
+        attend_row(q + r * D, Kbh, Vbh, clamp_len(src_len[b], S), D, out + r * D);
     }
     return 0;
 }
@@ -272,6 +315,63 @@ int oracle_ngram_block(const int32_t *tokens, int ld, int rows, int t, int n,
         }
     }
     return 0;
+}
+
+/*
+ * The bans of oracle_ngram_block as a list instead of writes: the pairs
+ * (row r, token v), v in [0, V), such that some window j in [0, t-n] of row r
+ * matches the row's last n-1 tokens and is followed by v.  Pairs are listed
+ * by row, then by increasing v, each once; pairs[2p] = r, pairs[2p+1] = v.
+ * At most max_pairs pairs are written; the return value is the number of
+ * pairs (which may exceed max_pairs), or -1 for invalid arguments.
+ */
+static int cmp_i32(const void *a, const void *b)
+{
+    const int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+long oracle_ngram_banned(const int32_t *tokens, int ld, int rows, int t, int n, int V,
+                         int32_t *pairs, long max_pairs)
+{
+    if (rows < 0 || t < 0 || n < 1 || V < 0 || ld < t || max_pairs < 0)
+        return -1;
+    if (rows == 0 || t < n)
+        return 0;
+    if (!tokens || (max_pairs > 0 && !pairs))
+        return -1;
+    int32_t *found = (int32_t *)malloc(sizeof(int32_t) * (size_t)(t - n + 1));
+    if (!found) abort();
+    long count = 0;
+    for (int r = 0; r < rows; ++r) {
+        const int32_t *x = tokens + (size_t)r * ld;
+        const int suffix = t - n + 1;
+        int nf = 0;
+        for (int j = 0; j <= t - n; ++j) {
+            int same = 1;
+            for (int c = 0; c < n - 1; ++c) {
+                if (x[j + c] != x[suffix + c]) {
+                    same = 0;
+                    break;
+                }
+            }
+            const int32_t v = x[j + n - 1];
+            if (same && v >= 0 && v < V)
+                found[nf++] = v;
+        }
+        qsort(found, (size_t)nf, sizeof(int32_t), cmp_i32);
+        for (int f = 0; f < nf; ++f) {
+            if (f > 0 && found[f] == found[f - 1])
+                continue;
+            if (count < max_pairs) {
+                pairs[2 * count] = r;
+                pairs[2 * count + 1] = found[f];
+            }
+            ++count;
+        }
+    }
+    free(found);
+    return count;
 }
 
 /*

@@ -20,6 +20,10 @@ FS_ERR_UNSUPPORTED = 2
 FS_ERR_HIP = 3
 FS_F32 = 0
 FS_BF16 = 1
+FS_TUNE_ATTN_PATH = 1
+FS_TUNE_SELECT_SLICES = 2
+FS_TUNE_VALIDATE = 3
+ATTN_PATHS = {"auto": 0, "split": 1, "whole1": 2, "whole2": 3, "whole4": 4}
 
 # (name, restype, argtypes) for every exported entry point.
 _c_int, _c_size, _vp = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
@@ -34,6 +38,9 @@ SIGNATURES = [
     ("fs_beam_prefix_attn", _c_int,
      [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
     ("fs_ngram_block", _c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp]),
+    ("fs_beam_decode_step", _c_int,
+     [_vp] * 5 + [_c_int] * 6 + [_vp] + [_c_int] * 3 + [_vp, _c_int, _vp, _c_size, _vp]),
+    ("fs_set_tuning", _c_int, [_c_int, _c_int]),
     ("fs_beam_select_workspace_bytes", _c_size, [_c_int] * 4),
     ("fs_beam_select", _c_int,
      [_vp, _vp, _vp, _c_int, _c_int, _c_int, _vp, _vp, _vp] + [_c_int] * 4 + [_vp, _c_size, _vp]),

@@ -117,6 +117,105 @@ def beam_cross_attn(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: 
     return out
 
 
+def beam_decode_step(q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, src_len: torch.Tensor,
+                     tokens: torch.Tensor, n: int, logits: torch.Tensor, t: int | None = None,
+                     out: torch.Tensor | None = None,
+                     workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """The decode step in one launch: :func:`beam_cross_attn` and
+    :func:`ngram_block` on the step's B*k hypotheses (tokens [B*k, ld],
+    logits [B*k, vocab], modified in place).  Bit for bit the two calls.
+    Returns ``out``."""
+    for name, x in (("q", q), ("K", K), ("V", V), ("src_len", src_len)):
+        _need_cuda(name, x)
+    _need_cuda("logits", logits)
+    if q.dim() != 4 or K.dim() != 4 or K.shape != V.shape:
+        raise ValueError("q must be [B,k,H,D] and K, V [B,H,S,D]")
+    B, k, H, D = q.shape
+    if K.shape[0] != B or K.shape[1] != H or K.shape[3] != D:
+        raise ValueError(f"shape mismatch: q{tuple(q.shape)} K{tuple(K.shape)}")
+    S = K.shape[2]
+    dt = _DTYPES.get(q.dtype)
+    if dt is None or K.dtype != q.dtype or V.dtype != q.dtype:
+        raise ValueError("q, K and V must all be float32 or all bfloat16")
+    if src_len.dtype != torch.int32 or src_len.shape != (B,):
+        raise ValueError("src_len must be int32 [B]")
+    if not isinstance(tokens, torch.Tensor) or tokens.device.type != "cuda":
+        raise ValueError("tokens must be a GPU tensor")
+    if tokens.dim() != 2 or tokens.dtype != torch.int32 or tokens.shape[0] != B * k:
+        raise ValueError("tokens must be int32 [B*k, ld]")
+    rows, cols = tokens.shape
+    if rows > 0 and cols > 1 and tokens.stride(1) != 1:
+        raise ValueError("tokens must have unit column stride")
+    if logits.dim() != 2 or logits.dtype != torch.float32 or logits.shape[0] != rows:
+        raise ValueError("logits must be float32 [B*k, vocab]")
+    dev = q.device
+    if any(x.device != dev for x in (K, V, src_len, tokens, logits)):
+        raise ValueError("all tensors must be on one device")
+    ld = tokens.stride(0) if rows > 1 else cols
+    if t is None:
+        t = cols
+    if t > cols:
+        raise ValueError("t exceeds the columns of tokens")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _need_cuda("out", out)
+        if out.shape != q.shape or out.dtype != q.dtype or out.device != dev:
+            raise ValueError("out must match q in shape, dtype and device")
+    if workspace is None:
+        workspace = new_workspace(beam_cross_attn_workspace_bytes(B, k, H, S, D, q.dtype), dev)
+    else:
+        _need_cuda("workspace", workspace)
+    with _on(dev):
+        _N.check(_N.ext().fs_beam_decode_step(
+            q.data_ptr(), K.data_ptr(), V.data_ptr(), src_len.data_ptr(), out.data_ptr(),
+            B, k, H, S, D, dt, tokens.data_ptr(), ld, int(t), int(n), logits.data_ptr(), logits.shape[1],
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream_ptr(dev)))
+    return out
+
+
+def set_tuning(knob: int, value: int) -> int:
+    """fs_set_tuning: replace a size rule for every later call in the
+    process; returns the previous value."""
+    prev = _N.lib().fs_set_tuning(int(knob), int(value))
+    if prev < 0:
+        raise ValueError(f"unknown tuning knob {knob} or value {value}")
+    return prev
+
+
+@contextlib.contextmanager
+def attn_path(name: str):
+    """Force one decomposition of the attention calls inside the block
+    ('auto', 'split', 'whole1', 'whole2', 'whole4'); every decomposition
+    gives the same bits."""
+    prev = set_tuning(_N.FS_TUNE_ATTN_PATH, _N.ATTN_PATHS[name])
+    try:
+        yield
+    finally:
+        set_tuning(_N.FS_TUNE_ATTN_PATH, prev)
+
+
+@contextlib.contextmanager
+def validate_lengths(on: bool = True):
+    """Debug mode inside the block: the attention calls copy the lengths to
+    the host and reject out-of-range ones (FS_VALIDATE)."""
+    prev = set_tuning(_N.FS_TUNE_VALIDATE, int(on))
+    try:
+        yield
+    finally:
+        set_tuning(_N.FS_TUNE_VALIDATE, prev)
+
+
+@contextlib.contextmanager
+def select_slices(n: int):
+    """Force fs_beam_select's vocabulary slice count inside the block (0: the size rule)."""
+    prev = set_tuning(_N.FS_TUNE_SELECT_SLICES, n)
+    try:
+        yield
+    finally:
+        set_tuning(_N.FS_TUNE_SELECT_SLICES, prev)
+
+
 def beam_prefix_attn_workspace_bytes(B: int, k: int, H: int, N: int, T: int, D: int,
                                      dtype: torch.dtype = torch.bfloat16) -> int:
     """Bytes of workspace fs_beam_prefix_attn needs for these sizes."""

@@ -36,6 +36,8 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <atomic>
+
 
 #include "launch.h"
 
@@ -691,19 +693,24 @@ __global__ __launch_bounds__(kThreads) void beam_select_kernel(
 
 }  // namespace
 
+namespace {
+std::atomic<int> g_slices_override{0};
+}  // namespace
+
+int set_select_slices_override(int slices) {
+    return g_slices_override.exchange(slices > 0 ? slices : 0, std::memory_order_relaxed);
+}
+
 int beam_select_slices(int rows, int V, int k, int c) {
     // About kTargetWorkgroups slice workgroups, slices of at least 1024
     // logits, and no more than one merger ranks; a slice's window (slice plus
     // up to 3 leading positions) fits the kSliceMax positions of a workgroup.
-    // FS_SELECT_SLICES (read once) sets the count within the same limits.
+    // set_select_slices_override sets the count within the same limits.
     constexpr int kTargetWorkgroups = 512;
     const int by_size = (V + kSliceMax - 4) / (kSliceMax - 3);
     const int by_cand = kMergeCap / (k * c > 0 ? k * c : 1);
     const int by_words = kMergeWords / (k * rec_words(c) > 0 ? k * rec_words(c) : 1);
-    static const int forced = [] {
-        const char *e = getenv("FS_SELECT_SLICES");
-        return e ? atoi(e) : 0;
-    }();
+    const int forced = g_slices_override.load(std::memory_order_relaxed);
     int ns = forced > 0 ? forced : (kTargetWorkgroups + rows - 1) / (rows > 0 ? rows : 1);
     if (forced <= 0) ns = ns < (V + 1023) / 1024 ? ns : (V + 1023) / 1024;
     ns = ns < by_cand ? ns : by_cand;

@@ -44,12 +44,19 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb) {
     return pa < pb + nb && pb < pa + na;
 }
 
+// Debug mode: FS_VALIDATE=1 in the environment when the library is first
+// used, or fs_set_tuning(FS_TUNE_VALIDATE, 1).
+std::atomic<int> g_validate{-1};   // -1: not read from the environment yet
+
 bool validate_mode() {
-    static const bool on = [] {
-        const char *v = std::getenv("FS_VALIDATE");
-        return v && v[0] == '1';
-    }();
-    return on;
+    int v = g_validate.load(std::memory_order_relaxed);
+    if (v < 0) {
+        const char *e = std::getenv("FS_VALIDATE");
+        int expected = -1;
+        g_validate.compare_exchange_strong(expected, (e && e[0] == '1') ? 1 : 0, std::memory_order_relaxed);
+        v = g_validate.load(std::memory_order_relaxed);
+    }
+    return v == 1;
 }
 
 // Epochs tag the partial records in the workspace: every call gets a fresh
@@ -66,6 +73,14 @@ unsigned long long next_epoch() {
 
 bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
 
+// Largest (source, head) block of K or V, in bytes: the kernels address one
+// block through a 32-bit buffer range.
+constexpr long long kMaxBlockBytes = 0x7ff00000LL;
+
+static_assert((int)fs::AttnPath::kSplit == FS_ATTN_PATH_SPLIT && (int)fs::AttnPath::kWhole1 == FS_ATTN_PATH_WHOLE1 &&
+                  (int)fs::AttnPath::kWhole2 == FS_ATTN_PATH_WHOLE2 && (int)fs::AttnPath::kWhole4 == FS_ATTN_PATH_WHOLE4,
+              "the tuning values name the decompositions");
+
 // A call whose kernels exchange tagged records through the workspace tells
 // its own records from older ones by a tag passed at launch.  Under stream
 // capture that tag would be frozen into the graph, and a replay could take
@@ -75,12 +90,28 @@ bool capturing(hipStream_t s) {
     return hipStreamIsCapturing(s, &st) == hipSuccess && st != hipStreamCaptureStatusNone;
 }
 
-// Whether an attention call of n_bh rows over S keys (plus a generated-token
-// job) takes the decomposition that exchanges records.
-bool attn_uses_records(int n_bh, int S, int D, int esize, bool gen_job) {
+// Decomposition of an attention call of n_bh rows over S keys (plus a
+// generated-token job); chosen once per call.
+fs::AttnPath attn_path_for(int n_bh, int S, int D, int esize, bool gen_job) {
     const int C = fs::cross_attn_chunk_keys(D, esize);
     const int NC = std::max(1, (S + C - 1) / C);
-    return fs::choose_attn_path(n_bh, NC + (gen_job ? 1 : 0)) == fs::AttnPath::kSplit;
+    return fs::choose_attn_path(n_bh, NC + (gen_job ? 1 : 0));
+}
+
+// FS_VALIDATE's check of the device-resident lengths: a synchronous copy to
+// the host, refused while the stream is capturing (the copy and the
+// synchronisation would end the capture).
+int validate_lengths(const int32_t *len, int B, int limit, hipStream_t s, const char *what) {
+    if (capturing(s))
+        return fail(FS_ERR_UNSUPPORTED, "FS_VALIDATE copies %s to the host, which a capturing stream cannot do", what);
+    std::vector<int32_t> lens((size_t)B);
+    hipError_t e = hipMemcpyAsync(lens.data(), len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(FS_ERR_HIP, "FS_VALIDATE copy of %s: %s (%d)", what, hipGetErrorString(e), (int)e);
+    for (int b = 0; b < B; ++b)
+        if (lens[b] < 0 || lens[b] > limit)
+            return fail(FS_ERR_INVALID_ARG, "%s[%d] = %d outside [0, %d]", what, b, lens[b], limit);
+    return FS_OK;
 }
 
 // Host-side shape checks shared by the workspace query and the launch.
@@ -96,9 +127,65 @@ int check_attn_sizes(int B, int k, int H, int S, int D, int dtype) {
     const long long C = fs::cross_attn_chunk_keys(D, esize);
     const long long nc = std::max(1LL, (S + C - 1) / C);
     const long long bh_padded = ((long long)B * H + 7) / 8 * 8;  // chunk grid is padded to 8 XCDs
-    if ((long long)B * k * H > INT_MAX || bh_padded * (nc + 2) > INT_MAX)
+    if ((long long)B * k * H > INT_MAX || bh_padded * (nc + 2) + (long long)B * k > INT_MAX)
         return fail(FS_ERR_INVALID_ARG, "problem too large for one launch (B=%d k=%d H=%d S=%d)",
                     B, k, H, S);
+    // one (source, head) block of K or V is read through a 32-bit byte range
+    if ((long long)S * D * esize > kMaxBlockBytes)
+        return fail(FS_ERR_UNSUPPORTED, "one (source, head) block of S*D = %lld elements exceeds 2 GiB",
+                    (long long)S * D);
+    return FS_OK;
+}
+
+// Checks of fs_beam_cross_attn's arguments (also the attention half of the
+// fused decode step); FS_OK or an error with g_last_error set.
+int check_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len, void *out, int B,
+                     int k, int H, int S, int D, int dtype, void *workspace, size_t workspace_bytes) {
+    const size_t esize = dtype == FS_BF16 ? 2 : 4;
+    const size_t q_bytes = (size_t)B * k * H * D * esize;
+    const size_t kv_bytes = (size_t)B * H * S * D * esize;
+    if (!q || !out || !src_len || (kv_bytes > 0 && (!K || !V)))
+        return fail(FS_ERR_INVALID_ARG, "null pointer (q=%p K=%p V=%p src_len=%p out=%p)",
+                    q, K, V, (const void *)src_len, out);
+    if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16))
+        return fail(FS_ERR_INVALID_ARG, "q, K, V and out must be 16-byte aligned");
+    if (!aligned(src_len, 4)) return fail(FS_ERR_INVALID_ARG, "src_len must be 4-byte aligned");
+    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, K, kv_bytes) ||
+        overlaps(out, q_bytes, V, kv_bytes) || overlaps(out, q_bytes, src_len, (size_t)B * 4))
+        return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
+    const size_t need = fs::cross_attn_workspace_floats(B, k, H, S, D, (int)esize, false) * sizeof(float);
+    if (workspace_bytes < need || (need > 0 && !workspace))
+        return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed",
+                    workspace_bytes, workspace, need);
+    if (!aligned(workspace, 16)) return fail(FS_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+    if (need > 0 && (overlaps(workspace, need, q, q_bytes) || overlaps(workspace, need, K, kv_bytes) ||
+                     overlaps(workspace, need, V, kv_bytes) || overlaps(workspace, need, out, q_bytes) ||
+                     overlaps(workspace, need, src_len, (size_t)B * 4)))
+        return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
+    return FS_OK;
+}
+
+// Checks of fs_ngram_block's arguments that do not depend on the work being
+// empty; FS_OK or an error with g_last_error set.
+int check_ngram_sizes(int ld_tokens, int rows, int t, int n, int V) {
+    if (rows < 0 || t < 0 || V < 0 || ld_tokens < 0)
+        return fail(FS_ERR_INVALID_ARG, "negative size (rows=%d t=%d V=%d ld=%d)", rows, t, V, ld_tokens);
+    if (n < 1) return fail(FS_ERR_INVALID_ARG, "n=%d < 1", n);
+    if (ld_tokens < t) return fail(FS_ERR_INVALID_ARG, "ld_tokens=%d < t=%d", ld_tokens, t);
+    return FS_OK;
+}
+
+// Checks of the n-gram buffers when there is work (rows > 0, t >= n).
+int check_ngram_buffers(const int32_t *tokens, int ld_tokens, int rows, int t, const float *logits, int V) {
+    if (!tokens || (V > 0 && !logits))
+        return fail(FS_ERR_INVALID_ARG, "null pointer (tokens=%p logits=%p)", (const void *)tokens,
+                    (const void *)logits);
+    if (!aligned(tokens, 4) || !aligned(logits, 4))
+        return fail(FS_ERR_INVALID_ARG, "tokens and logits must be 4-byte aligned");
+    const size_t tok_bytes = ((size_t)(rows - 1) * ld_tokens + t) * 4;
+    const size_t lg_bytes = (size_t)rows * V * 4;
+    if (overlaps(tokens, tok_bytes, logits, lg_bytes))
+        return fail(FS_ERR_INVALID_ARG, "logits overlap tokens");
     return FS_OK;
 }
 
@@ -148,46 +235,94 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
     int st = check_attn_sizes(B, k, H, S, D, dtype);
     if (st != FS_OK) return st;
     if (B == 0 || k == 0 || H == 0) return FS_OK;
-
-    const size_t esize = dtype == FS_BF16 ? 2 : 4;
-    const size_t q_bytes = (size_t)B * k * H * D * esize;
-    const size_t kv_bytes = (size_t)B * H * S * D * esize;
-    if (!q || !out || !src_len || (kv_bytes > 0 && (!K || !V)))
-        return fail(FS_ERR_INVALID_ARG, "null pointer (q=%p K=%p V=%p src_len=%p out=%p)",
-                    q, K, V, (const void *)src_len, out);
-    if (!aligned(q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(out, 16))
-        return fail(FS_ERR_INVALID_ARG, "q, K, V and out must be 16-byte aligned");
-    if (!aligned(src_len, 4)) return fail(FS_ERR_INVALID_ARG, "src_len must be 4-byte aligned");
-    if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, K, kv_bytes) ||
-        overlaps(out, q_bytes, V, kv_bytes) || overlaps(out, q_bytes, src_len, (size_t)B * 4))
-        return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
-    const size_t need = fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype);
-    if (workspace_bytes < need || (need > 0 && !workspace))
-        return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed",
-                    workspace_bytes, workspace, need);
-    if (!aligned(workspace, 16)) return fail(FS_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
-    if (need > 0 && (overlaps(workspace, need, q, q_bytes) || overlaps(workspace, need, K, kv_bytes) ||
-                     overlaps(workspace, need, V, kv_bytes) || overlaps(workspace, need, out, q_bytes) ||
-                     overlaps(workspace, need, src_len, (size_t)B * 4)))
-        return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
+    st = check_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype, workspace, workspace_bytes);
+    if (st != FS_OK) return st;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (attn_uses_records(B * H, S, D, (int)esize, false) && capturing(s))
+    const int esize = dtype == FS_BF16 ? 2 : 4;
+    const fs::AttnPath path = attn_path_for(B * H, S, D, esize, false);
+    if (path == fs::AttnPath::kSplit && capturing(s))
         return fail(FS_ERR_UNSUPPORTED, "fs_beam_cross_attn: %d rows take the split-KV form, whose tagged records "
                     "cannot be captured into a graph", B * H);
-    if (validate_mode()) {
-        std::vector<int32_t> lens((size_t)B);
-        hipError_t e = hipMemcpyAsync(lens.data(), src_len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
-        if (e == hipSuccess) e = hipStreamSynchronize(s);
-        if (e != hipSuccess) return hip_fail(e, "FS_VALIDATE copy of src_len");
-        for (int b = 0; b < B; ++b)
-            if (lens[b] < 0 || lens[b] > S)
-                return fail(FS_ERR_INVALID_ARG, "src_len[%d] = %d outside [0, %d]", b, lens[b], S);
-    }
+    if (validate_mode() && (st = validate_lengths(src_len, B, S, s, "src_len")) != FS_OK) return st;
     hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
-                                         static_cast<float *>(workspace), next_epoch(), s);
+                                         static_cast<float *>(workspace), next_epoch(), s, path);
     if (e != hipSuccess) return hip_fail(e, "fs_beam_cross_attn launch");
     return FS_OK;
+}
+
+int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32_t *src_len, void *out,
+                        int B, int k, int H, int S, int D, int dtype,
+                        const int32_t *tokens, int ld_tokens, int t, int n, float *logits, int vocab,
+                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    g_last_error.clear();
+    int st = check_attn_sizes(B, k, H, S, D, dtype);
+    if (st != FS_OK) return st;
+    const long long rows_ll = (long long)B * k;
+    if ((st = check_ngram_sizes(ld_tokens, (int)std::min<long long>(rows_ll, INT_MAX), t, n, vocab)) != FS_OK)
+        return st;
+    const int rows = (int)rows_ll;
+    const bool attn = B > 0 && k > 0 && H > 0;
+    const bool ngram = rows > 0 && t >= n && vocab > 0;
+    if (attn && (st = check_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype, workspace, workspace_bytes)) != FS_OK)
+        return st;
+    if (ngram) {
+        if ((st = check_ngram_buffers(tokens, ld_tokens, rows, t, logits, vocab)) != FS_OK) return st;
+        if (attn) {
+            // the two halves write disjoint buffers and read none of the other's outputs
+            const size_t esize = dtype == FS_BF16 ? 2 : 4;
+            const size_t q_bytes = (size_t)B * k * H * D * esize, kv_bytes = (size_t)B * H * S * D * esize;
+            const size_t lg_bytes = (size_t)rows * vocab * 4;
+            const size_t tok_bytes = ((size_t)(rows - 1) * ld_tokens + t) * 4;
+            const size_t ws_bytes = fs::cross_attn_workspace_floats(B, k, H, S, D, (int)esize, false) * sizeof(float);
+            if (overlaps(logits, lg_bytes, q, q_bytes) || overlaps(logits, lg_bytes, K, kv_bytes) ||
+                overlaps(logits, lg_bytes, V, kv_bytes) || overlaps(logits, lg_bytes, out, q_bytes) ||
+                overlaps(logits, lg_bytes, src_len, (size_t)B * 4) || overlaps(logits, lg_bytes, workspace, ws_bytes))
+                return fail(FS_ERR_INVALID_ARG, "logits overlap an attention argument");
+            if (overlaps(tokens, tok_bytes, out, q_bytes) || overlaps(tokens, tok_bytes, workspace, ws_bytes))
+                return fail(FS_ERR_INVALID_ARG, "tokens overlap out or the workspace");
+        }
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!attn) {
+        if (!ngram) return FS_OK;
+        hipError_t e = fs::launch_ngram_block(tokens, ld_tokens, rows, t, n, logits, vocab, s);
+        if (e != hipSuccess) return hip_fail(e, "fs_beam_decode_step n-gram launch");
+        return FS_OK;
+    }
+    const int esize = dtype == FS_BF16 ? 2 : 4;
+    const fs::AttnPath path = attn_path_for(B * H, S, D, esize, false);
+    if (path == fs::AttnPath::kSplit && capturing(s))
+        return fail(FS_ERR_UNSUPPORTED, "fs_beam_decode_step: %d rows take the split-KV form, whose tagged records "
+                    "cannot be captured into a graph", B * H);
+    if (validate_mode() && (st = validate_lengths(src_len, B, S, s, "src_len")) != FS_OK) return st;
+    const fs::NgramRows ng{tokens, ld_tokens, rows, t, n, logits, vocab};
+    hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
+                                         static_cast<float *>(workspace), next_epoch(), s, path,
+                                         ngram ? &ng : nullptr);
+    if (e != hipSuccess) return hip_fail(e, "fs_beam_decode_step launch");
+    return FS_OK;
+}
+
+int fs_set_tuning(int knob, int value)
+{
+    switch (knob) {
+    case FS_TUNE_ATTN_PATH:
+        if (value < 0 || value > FS_ATTN_PATH_WHOLE4) return -1;
+        return static_cast<int>(fs::set_attn_path_override(static_cast<fs::AttnPath>(value)));
+    case FS_TUNE_SELECT_SLICES:
+        if (value < 0) return -1;
+        return fs::set_select_slices_override(value);
+    case FS_TUNE_VALIDATE: {
+        if (value != 0 && value != 1) return -1;
+        const int prev = validate_mode() ? 1 : 0;
+        g_validate.store(value, std::memory_order_relaxed);
+        return prev;
+    }
+    default:
+        return -1;
+    }
 }
 
 }  // extern "C"
@@ -224,6 +359,9 @@ int prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *pr
         return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
     if ((long long)B * k * H * ((long long)T * D) > (long long)INT_MAX * 16)
         return fail(FS_ERR_INVALID_ARG, "generated-token cache too large");
+    if ((long long)T * D * (long long)esize > kMaxBlockBytes)
+        return fail(FS_ERR_UNSUPPORTED, "one (hypothesis, head) block of T*D = %lld generated elements exceeds 2 GiB",
+                    (long long)T * D);
     if (indirect && t > 0) {
         if (!anc) return fail(FS_ERR_INVALID_ARG, "null ancestry table with t=%d > 0", t);
         if (ld_anc < t) return fail(FS_ERR_INVALID_ARG, "ld_anc=%d < t=%d", ld_anc, t);
@@ -247,21 +385,14 @@ int prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *pr
         return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
 
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (attn_uses_records(B * H, N, D, dtype == FS_BF16 ? 2 : 4, t > 0) && capturing(s))
+    const fs::AttnPath path = attn_path_for(B * H, N, D, dtype == FS_BF16 ? 2 : 4, t > 0);
+    if (path == fs::AttnPath::kSplit && capturing(s))
         return fail(FS_ERR_UNSUPPORTED, "%d rows take the split-KV form, whose tagged records cannot be captured "
                     "into a graph", B * H);
-    if (validate_mode()) {
-        std::vector<int32_t> lens((size_t)B);
-        hipError_t e = hipMemcpyAsync(lens.data(), prefix_len, (size_t)B * 4, hipMemcpyDeviceToHost, s);
-        if (e == hipSuccess) e = hipStreamSynchronize(s);
-        if (e != hipSuccess) return hip_fail(e, "FS_VALIDATE copy of prefix_len");
-        for (int b = 0; b < B; ++b)
-            if (lens[b] < 0 || lens[b] > N)
-                return fail(FS_ERR_INVALID_ARG, "prefix_len[%d] = %d outside [0, %d]", b, lens[b], N);
-    }
+    if (validate_mode() && (st = validate_lengths(prefix_len, B, N, s, "prefix_len")) != FS_OK) return st;
     hipError_t e = fs::launch_prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, T, t, indirect && t > 0 ? anc : nullptr,
                                           ld_anc, out, B, k, H, N, D, dtype == FS_BF16,
-                                          static_cast<float *>(workspace), next_epoch(), s);
+                                          static_cast<float *>(workspace), next_epoch(), s, path);
     if (e != hipSuccess) return hip_fail(e, indirect ? "fs_beam_prefix_attn_indirect launch" : "fs_beam_prefix_attn launch");
     return FS_OK;
 }
@@ -312,20 +443,10 @@ int fs_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t, int n,
                    float *logits, int V, void *stream)
 {
     g_last_error.clear();
-    if (rows < 0 || t < 0 || V < 0 || ld_tokens < 0)
-        return fail(FS_ERR_INVALID_ARG, "negative size (rows=%d t=%d V=%d ld=%d)", rows, t, V, ld_tokens);
-    if (n < 1) return fail(FS_ERR_INVALID_ARG, "n=%d < 1", n);
-    if (ld_tokens < t) return fail(FS_ERR_INVALID_ARG, "ld_tokens=%d < t=%d", ld_tokens, t);
+    int st = check_ngram_sizes(ld_tokens, rows, t, n, V);
+    if (st != FS_OK) return st;
     if (rows == 0 || t < n) return FS_OK;  // no window: nothing to ban
-    if (!tokens || (V > 0 && !logits))
-        return fail(FS_ERR_INVALID_ARG, "null pointer (tokens=%p logits=%p)", (const void *)tokens,
-                    (void *)logits);
-    if (!aligned(tokens, 4) || !aligned(logits, 4))
-        return fail(FS_ERR_INVALID_ARG, "tokens and logits must be 4-byte aligned");
-    const size_t tok_bytes = ((size_t)(rows - 1) * ld_tokens + t) * 4;
-    const size_t lg_bytes = (size_t)rows * V * 4;
-    if (overlaps(tokens, tok_bytes, logits, lg_bytes))
-        return fail(FS_ERR_INVALID_ARG, "logits overlap tokens");
+    if ((st = check_ngram_buffers(tokens, ld_tokens, rows, t, logits, V)) != FS_OK) return st;
     if (V == 0) return FS_OK;  // no id is in range: nothing can be written
     hipError_t e = fs::launch_ngram_block(tokens, ld_tokens, rows, t, n, logits, V,
                                           static_cast<hipStream_t>(stream));

@@ -37,9 +37,11 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "launch.h"
+#include "ngram_row.h"
 
 namespace fs {
 namespace {
@@ -926,12 +928,19 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     unsigned long long *__restrict__ part,
     int n_bh, int H, int S, int NC, float scale_log2, unsigned long long epoch,
     const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t, const int32_t *__restrict__ anc,
-    int ld_anc)
+    int ld_anc, NgramJob ngj)
 {
     using G = Geo<D, BF16>;
     using TL = Tile<D, BF16, KB>;
     constexpr int kLpr = G::kLpr;
     constexpr int kTile = G::kTile, kChunk = G::kChunk;
+
+    // A fused decode step's n-gram rows take the first workgroups (a
+    // multiple of 8, so the XCD residues of the ids below are kept).
+    if ((int)blockIdx.x < ngj.blocks) {
+        ngram_job_block(ngj, blockIdx.x, kWaves);
+        return;
+    }
 
     __shared__ float m_lds[kWaves][KB], l_lds[kWaves][KB];
     // each wave's tile area, which then holds its acc[KB][D] for the merge
@@ -944,7 +953,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     // generated-token workgroups (SPLIT only; each walks its tiles in
     // sequence, so they start first), the chunk workgroups, the mergers.
     const int n_bh8 = ((n_bh + kXcds - 1) / kXcds) * kXcds;
-    int g = blockIdx.x;
+    int g = blockIdx.x - ngj.blocks;
     if constexpr (SPLIT) {
         if (g < n_bh8) {
             attend_generated<D, BF16, KB, ANC>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
@@ -1038,7 +1047,7 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     const uint4 *__restrict__ q, const uint4 *__restrict__ K, const uint4 *__restrict__ V,
     const int32_t *__restrict__ src_len, void *__restrict__ out, int n_bh, int H, int S,
     float scale_log2, const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t,
-    const int32_t *__restrict__ anc, int ld_anc)
+    const int32_t *__restrict__ anc, int ld_anc, NgramJob ngj)
 {
     using G = Geo<D, BF16>;
     using TL = Tile<D, BF16, KB>;
@@ -1056,7 +1065,12 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     __shared__ __attribute__((aligned(16))) float g_lds[kGB][kGD];
     __shared__ float gm_lds[kGB], gl_lds[kGB];
 
-    const int bh = blockIdx.x;
+    // A fused decode step's n-gram rows take the first workgroups.
+    if ((int)blockIdx.x < ngj.blocks) {
+        ngram_job_block(ngj, blockIdx.x, kW);
+        return;
+    }
+    const int bh = blockIdx.x - ngj.blocks;
     if (bh >= n_bh) return;
     const int b = bh / H;
     const int h = bh - b * H;
@@ -1196,6 +1210,8 @@ struct AttnArgs {
     float *ws;
     unsigned long long epoch;
     hipStream_t stream;
+    NgramJob ng;          // n-gram rows of a fused decode step (ng.rows == 0: none)
+    AttnPath path;        // decomposition chosen for the call
 };
 
 template <int D, bool BF16, int KB, bool SPLIT, bool ANC = false>
@@ -1207,12 +1223,17 @@ hipError_t launch_split(const AttnArgs &a, int NC)
     unsigned long long *part = reinterpret_cast<unsigned long long *>(a.ws);
     // [generated-token workgroups] [chunk workgroups] [mergers]
     const long long mergers = (SPLIT || NC > 1) ? n_bh : 0;
-    const long long nblk = (SPLIT ? n_bh8 : 0) + n_bh8 * NC + mergers;
+    // n-gram workgroups first, rounded to a multiple of 8 so that the XCD
+    // residues of the ids after them are kept
+    NgramJob ng = a.ng;
+    ng.blocks = ng.rows > 0 ? (ng.rows + kWaves - 1) / kWaves : 0;
+    ng.blocks = (ng.blocks + kXcds - 1) / kXcds * kXcds;
+    const long long nblk = ng.blocks + (SPLIT ? n_bh8 : 0) + n_bh8 * NC + mergers;
     hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB, SPLIT, ANC>), dim3((unsigned)nblk), dim3(kBlock), 0,
                        a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
                        static_cast<const uint4 *>(a.V), a.src_len, a.out, part, n_bh, a.H, a.S,
                        NC, (float)scale_log2, a.epoch, static_cast<const uint4 *>(a.Kt),
-                       static_cast<const uint4 *>(a.Vt), a.T, a.t, a.anc, a.ld_anc);
+                       static_cast<const uint4 *>(a.Vt), a.T, a.t, a.anc, a.ld_anc, ng);
     return hipGetLastError();
 }
 
@@ -1221,11 +1242,14 @@ hipError_t launch_whole(const AttnArgs &a)
 {
     const int n_bh = a.B * a.H;
     const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
-    hipLaunchKernelGGL((attn_whole_kernel<D, BF16, KB, SPLIT, P, ANC>), dim3((unsigned)n_bh), dim3(kBlock * P), 0,
+    NgramJob ng = a.ng;
+    ng.blocks = ng.rows > 0 ? (ng.rows + kWaves * P - 1) / (kWaves * P) : 0;
+    hipLaunchKernelGGL((attn_whole_kernel<D, BF16, KB, SPLIT, P, ANC>), dim3((unsigned)(ng.blocks + n_bh)),
+                       dim3(kBlock * P), 0,
                        a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
                        static_cast<const uint4 *>(a.V), a.src_len, a.out, n_bh, a.H, a.S, (float)scale_log2,
                        static_cast<const uint4 *>(a.Kt), static_cast<const uint4 *>(a.Vt), a.T, a.t, a.anc,
-                       a.ld_anc);
+                       a.ld_anc, ng);
     return hipGetLastError();
 }
 
@@ -1236,8 +1260,7 @@ hipError_t launch_typed(const AttnArgs &a)
     // at least one chunk column, so that a source with no valid key (or
     // S == 0) still has a workgroup to write its zero output
     const int NC = max(1, (a.S + G::kChunk - 1) / G::kChunk);
-    // jobs per row: its chunks, plus the generated tokens of the split cache
-    const AttnPath path = choose_attn_path(a.B * a.H, NC + (SPLIT && a.t > 0 ? 1 : 0));
+    const AttnPath path = a.path;
     if constexpr (SPLIT) {
         if (a.anc) {
             // generated rows through the ancestry table: their own kernels,
@@ -1288,13 +1311,17 @@ hipError_t launch_d(const AttnArgs &a)
 
 }  // namespace
 
+namespace {
+std::atomic<int> g_path_override{0};
+}  // namespace
+
+AttnPath set_attn_path_override(AttnPath p) {
+    return static_cast<AttnPath>(g_path_override.exchange(static_cast<int>(p), std::memory_order_relaxed));
+}
+
 AttnPath choose_attn_path(int n_bh, int jobs_max) {
-    if (const char *v = getenv("FS_ATTN_PATH")) {
-        if (!strcmp(v, "split")) return AttnPath::kSplit;
-        if (!strcmp(v, "whole1")) return AttnPath::kWhole1;
-        if (!strcmp(v, "whole2")) return AttnPath::kWhole2;
-        if (!strcmp(v, "whole4")) return AttnPath::kWhole4;
-    }
+    const AttnPath forced = static_cast<AttnPath>(g_path_override.load(std::memory_order_relaxed));
+    if (forced != AttnPath::kAuto) return forced;
     // Measured on MI355X (bf16, D = 64, k = 4 or 5; 192 to 5120 rows of up to
     // 1024 keys): an 8-wave workgroup per row (two jobs in flight) is the
     // fastest from 256 rows up (BART-shaped 512 rows: 18.6 us against 19.5
@@ -1325,18 +1352,23 @@ size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize,
 
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len,
                              void *out, int B, int k, int H, int S, int D, bool bf16,
-                             float *workspace, unsigned long long epoch, hipStream_t stream)
+                             float *workspace, unsigned long long epoch, hipStream_t stream,
+                             AttnPath path, const NgramRows *ngram)
 {
-    const AttnArgs a{q, K, V, src_len, out, B, k, H, S, D, nullptr, nullptr, 0, 0, nullptr, 0, workspace, epoch, stream};
+    AttnArgs a{q, K, V, src_len, out, B, k, H, S, D, nullptr, nullptr, 0, 0, nullptr, 0, workspace, epoch, stream,
+               NgramJob{nullptr, nullptr, 0, 0, 0, 0, 0, 0}, path};
+    if (ngram)
+        a.ng = NgramJob{ngram->tokens, ngram->logits, ngram->ld, ngram->t, ngram->n - 1, ngram->V, ngram->rows, 0};
     return bf16 ? launch_d<true, false>(a) : launch_d<false, false>(a);
 }
 
 hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
                               const void *Kt, const void *Vt, int T, int t, const int32_t *anc, int ld_anc,
                               void *out, int B, int k, int H, int N, int D, bool bf16, float *workspace,
-                              unsigned long long epoch, hipStream_t stream)
+                              unsigned long long epoch, hipStream_t stream, AttnPath path)
 {
-    const AttnArgs a{q, Kp, Vp, prefix_len, out, B, k, H, N, D, Kt, Vt, T, t, anc, ld_anc, workspace, epoch, stream};
+    const AttnArgs a{q, Kp, Vp, prefix_len, out, B, k, H, N, D, Kt, Vt, T, t, anc, ld_anc, workspace, epoch, stream,
+                     NgramJob{nullptr, nullptr, 0, 0, 0, 0, 0, 0}, path};
     return bf16 ? launch_d<true, true>(a) : launch_d<false, true>(a);
 }
 

@@ -23,21 +23,38 @@ int cross_attn_chunk_keys(int D, int esize);
 enum class AttnPath { kAuto = 0, kSplit, kWhole1, kWhole2, kWhole4 };
 
 // The path for n_bh = B*H rows of at most jobs_max jobs (chunks, plus the
-// generated tokens of the split cache): FS_ATTN_PATH
-// (split, whole1, whole2, whole4; read at every call) overrides the size rule.
+// generated tokens of the split cache): the size rule, unless a path was
+// forced with set_attn_path_override.
 AttnPath choose_attn_path(int n_bh, int jobs_max);
+
+// Process-wide overrides of the size rules, for tests and measurements
+// (fs_set_tuning).  kAuto / 0 restore the rules; each returns the previous value.
+AttnPath set_attn_path_override(AttnPath p);
+int set_select_slices_override(int slices);
 
 // Workspace size in 4-byte words: the per-chunk partial records (plus one
 // record per (b, h) for the generated-token segment when `split`).
 size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize, bool split);
 
+// The n-gram part of a fused decode step (the arguments of fs_ngram_block):
+// its rows are scanned by extra workgroups of the attention launch.
+struct NgramRows {
+    const int32_t *tokens;
+    int ld, rows, t, n;
+    float *logits;
+    int V;
+};
+
 // `epoch` must differ from the epoch of every earlier call that used the
 // same workspace: its low 32 bits tag the partial records, which are never
-// cleared.
+// cleared.  With `ngram` (rows > 0, t >= n) the launch also applies the
+// n-gram bans.
+// `path` is the decomposition choose_attn_path gave for the call.
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
                              const int32_t *src_len, void *out,
                              int B, int k, int H, int S, int D, bool bf16,
-                             float *workspace, unsigned long long epoch, hipStream_t stream);
+                             float *workspace, unsigned long long epoch, hipStream_t stream,
+                             AttnPath path, const NgramRows *ngram = nullptr);
 
 // Split-cache self-attention: shared prefix Kp/Vp [B,H,N,D] with
 // prefix_len[B], per-beam generated tokens Kt/Vt [B*k,H,T,D] (rows < t).
@@ -46,7 +63,7 @@ hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
 hipError_t launch_prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *prefix_len,
                               const void *Kt, const void *Vt, int T, int t, const int32_t *anc, int ld_anc,
                               void *out, int B, int k, int H, int N, int D, bool bf16, float *workspace,
-                              unsigned long long epoch, hipStream_t stream);
+                              unsigned long long epoch, hipStream_t stream, AttnPath path);
 
 hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, int t,
                               int n, float *logits, int V, hipStream_t stream);

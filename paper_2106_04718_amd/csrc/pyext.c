@@ -55,6 +55,17 @@ static PyObject *py_beam_cross_attn(PyObject *self, PyObject *const *args, Py_ss
     return PyLong_FromLong(st);
 }
 
+static PyObject *py_beam_decode_step(PyObject *self, PyObject *const *args, Py_ssize_t nargs) {
+    unsigned long long u[20];
+    int v[20];
+    (void)self;
+    if (unpack(args, nargs, "pppppiiiiiipiiipippp", u, v)) return NULL;
+    int st = fs_beam_decode_step(PTR(0), PTR(1), PTR(2), (const int32_t *)PTR(3), PTR(4), v[5], v[6], v[7], v[8],
+                                 v[9], v[10], (const int32_t *)PTR(11), v[12], v[13], v[14], (float *)PTR(15),
+                                 v[16], PTR(17), (size_t)u[18], PTR(19));
+    return PyLong_FromLong(st);
+}
+
 static PyObject *py_beam_prefix_attn(PyObject *self, PyObject *const *args, Py_ssize_t nargs) {
     unsigned long long u[19];
     int v[19];
@@ -125,6 +136,9 @@ static PyObject *py_last_error(PyObject *self, PyObject *unused) {
 static PyMethodDef methods[] = {
     {"fs_beam_cross_attn", (PyCFunction)(void (*)(void))py_beam_cross_attn, METH_FASTCALL,
      "fs_beam_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype, workspace, workspace_bytes, stream)"},
+    {"fs_beam_decode_step", (PyCFunction)(void (*)(void))py_beam_decode_step, METH_FASTCALL,
+     "fs_beam_decode_step(q, K, V, src_len, out, B, k, H, S, D, dtype, tokens, ld_tokens, t, n, logits, vocab, "
+     "workspace, workspace_bytes, stream)"},
     {"fs_beam_prefix_attn", (PyCFunction)(void (*)(void))py_beam_prefix_attn, METH_FASTCALL,
      "fs_beam_prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, T, t, out, B, k, H, N, D, dtype, workspace, "
      "workspace_bytes, stream)"},

@@ -277,3 +277,80 @@ def test_indirect_prefix_attn_rejects(kw, status, needle):
 def test_indirect_prefix_attn_needs_no_table_without_generated_tokens():
     # t == 0 reads no table: a null anc passes validation (and B == 0 launches nothing)
     assert indirect(anc=None, t=0, B=0) == N.FS_OK
+
+
+def test_block_over_2gib_is_unsupported():
+    # one (source, head) block of K/V is read through a 32-bit byte range
+    f = N.lib().fs_beam_cross_attn_workspace_bytes
+    assert f(1, 1, 1, 1 << 24, 128, N.FS_BF16) == 2**64 - 1
+    assert "2 GiB" in N.last_error()
+    assert attn(B=1, k=1, H=1, S=1 << 24, D=128, dtype=N.FS_BF16) == N.FS_ERR_UNSUPPORTED
+    assert "2 GiB" in N.last_error()
+    # just under the limit passes the size checks (then fails on a null pointer, before any launch)
+    S = 0x7ff00000 // (128 * 2)
+    assert f(1, 1, 1, S, 128, N.FS_BF16) != 2**64 - 1
+    assert attn(B=1, k=1, H=1, S=S, D=128, dtype=N.FS_BF16, q=None) == N.FS_ERR_INVALID_ARG
+
+
+def test_prefix_generated_block_over_2gib_is_unsupported():
+    lib = N.lib()
+    T = (0x7ff00000 // (64 * 4)) + 1
+    far = 1 << 40   # the generated-token blocks span 2 GiB: keep every fake buffer apart
+    st = lib.fs_beam_prefix_attn(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, far, 2 * far, T, 1, 3 * far,
+                                 1, 1, 1, 16, 64, N.FS_F32, 4 * far, 1 << 30, None)
+    assert st == N.FS_ERR_UNSUPPORTED and "2 GiB" in N.last_error()
+
+
+def step(**kw):
+    a = dict(q=FAKE, K=FAKE * 2, V=FAKE * 3, src_len=FAKE * 4, out=FAKE * 5,
+             B=2, k=4, H=2, S=64, D=16, dtype=N.FS_F32, tokens=FAKE * 7, ld=8, t=8, n=3,
+             logits=FAKE * 8, vocab=100, ws=FAKE * 6, ws_bytes=1 << 16, stream=None)
+    a.update(kw)
+    return N.lib().fs_beam_decode_step(a["q"], a["K"], a["V"], a["src_len"], a["out"], a["B"], a["k"], a["H"],
+                                       a["S"], a["D"], a["dtype"], a["tokens"], a["ld"], a["t"], a["n"],
+                                       a["logits"], a["vocab"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(D=48), N.FS_ERR_UNSUPPORTED, "D=48"),
+    (dict(n=0), N.FS_ERR_INVALID_ARG, "n=0"),
+    (dict(ld=4), N.FS_ERR_INVALID_ARG, "ld_tokens"),
+    (dict(q=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(tokens=None), N.FS_ERR_INVALID_ARG, "null"),
+    (dict(out=FAKE * 2), N.FS_ERR_INVALID_ARG, "overlaps"),
+    (dict(logits=FAKE * 7 + 16), N.FS_ERR_INVALID_ARG, "overlap tokens"),
+    (dict(logits=FAKE * 5), N.FS_ERR_INVALID_ARG, "attention argument"),
+    (dict(logits=FAKE * 2 + 128), N.FS_ERR_INVALID_ARG, "attention argument"),
+    (dict(logits=FAKE * 6), N.FS_ERR_INVALID_ARG, "attention argument"),
+    (dict(tokens=FAKE * 5), N.FS_ERR_INVALID_ARG, "tokens overlap"),
+    (dict(ws_bytes=16), N.FS_ERR_INVALID_ARG, "workspace"),
+])
+def test_decode_step_rejects(kw, status, needle):
+    assert step(**kw) == status
+    assert needle in N.last_error()
+
+
+def test_decode_step_empty_halves_return_ok_without_launch():
+    # no attention and no n-gram window: nothing runs, nothing is read
+    nulls = dict(q=None, K=None, V=None, src_len=None, out=None, ws=None, ws_bytes=0, tokens=None, logits=None)
+    assert step(B=0, **nulls) == N.FS_OK
+    assert step(H=0, t=2, n=3, **nulls) == N.FS_OK
+    assert step(H=0, vocab=0, **nulls) == N.FS_OK
+
+
+def test_tuning_controls():
+    lib = N.lib()
+    assert lib.fs_set_tuning(99, 0) == -1
+    assert lib.fs_set_tuning(N.FS_TUNE_ATTN_PATH, 17) == -1
+    assert lib.fs_set_tuning(N.FS_TUNE_SELECT_SLICES, -3) == -1
+    prev = lib.fs_set_tuning(N.FS_TUNE_ATTN_PATH, N.ATTN_PATHS["whole1"])
+    assert prev == N.ATTN_PATHS["auto"]
+    assert lib.fs_set_tuning(N.FS_TUNE_ATTN_PATH, prev) == N.ATTN_PATHS["whole1"]
+    assert lib.fs_set_tuning(N.FS_TUNE_SELECT_SLICES, 5) == 0
+    assert lib.fs_set_tuning(N.FS_TUNE_SELECT_SLICES, 0) == 5
+    assert lib.fs_set_tuning(N.FS_TUNE_VALIDATE, 2) == -1
+    was = lib.fs_set_tuning(N.FS_TUNE_VALIDATE, 1)
+    assert lib.fs_set_tuning(N.FS_TUNE_VALIDATE, was) == 1
+    hdr = (ROOT / "include" / "fastseq_hip.h").read_text()
+    for name, v in N.ATTN_PATHS.items():
+        assert re.search(rf"FS_ATTN_PATH_{name.upper()} = {v}\b", hdr), name

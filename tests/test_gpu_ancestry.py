@@ -79,20 +79,13 @@ def decode(B, k, H, N, T, D, dtype, steps, seed, plen):
 def test_table_read_equals_the_reordered_cache_bitwise_on_every_path(dtype, D, k):
     B, H, N, T = 3, 2, 600, 80
     s = decode(B, k, H, N, T, D, dtype, steps=70, seed=D + k, plen=[600, 0, 257])
-    old = os.environ.get("FS_ATTN_PATH")
-    try:
-        for path in ("split", "whole1", "whole2", "whole4"):
-            os.environ["FS_ATTN_PATH"] = path
+    for path in ("split", "whole1", "whole2", "whole4"):
+        with api.attn_path(path):
             say(f"[indirect] {dtype} D={D} k={k} path={path}")
             direct = api.beam_prefix_attn(s["q"], s["Kp"], s["Vp"], s["pl"], s["Kr"], s["Vr"], s["t"])
             ind = api.beam_prefix_attn(s["q"], s["Kp"], s["Vp"], s["pl"], s["Ki"], s["Vi"], s["t"], anc=s["anc"])
             torch.cuda.synchronize()
             assert np.array_equal(bits(direct), bits(ind)), f"path={path}"
-    finally:
-        if old is None:
-            os.environ.pop("FS_ATTN_PATH", None)
-        else:
-            os.environ["FS_ATTN_PATH"] = old
     want = oracle.prefix_attn_indirect(to_host(s["q"]), to_host(s["Kp"]), to_host(s["Vp"]), s["pl"].cpu().numpy(),
                                        to_host(s["Ki"]), to_host(s["Vi"]), s["anc"].cpu().numpy(), s["t"])
     assert_attn_close(ind, want, f"indirect {dtype} D={D} k={k}")

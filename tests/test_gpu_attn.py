@@ -43,17 +43,19 @@ def test_config_parity_full(name):
     say(f"[attn parity] config={name} max_abs_err={err:.3e}")
 
 
-def test_large_config_parity_sampled_sources():
-    # B=320 at full size on the GPU; the oracle checks every 8th source
-    # (sources are independent, so each sampled output is exact to compute).
+def test_large_config_parity_every_source():
+    # B=320 at full size on the GPU in one launch; the oracle computes every
+    # source, 40 at a time (sources are independent) to bound host memory.
     cfg = workloads.get("large")
     say("[attn parity] config=large")
     d = workloads.attn_inputs(cfg)
     out = run(d)
-    idx = np.arange(0, cfg.B, 8)
-    sub = {"q": d["q"][idx], "K": d["K"][idx], "V": d["V"][idx], "src_len": d["src_len"][idx]}
-    err = assert_attn_close(out[idx.tolist()], oracle_attn(sub), "large")
-    say(f"[attn parity] config=large sampled max_abs_err={err:.3e}")
+    worst = 0.0
+    for b0 in range(0, cfg.B, 40):
+        idx = np.arange(b0, min(cfg.B, b0 + 40))
+        sub = {"q": d["q"][idx], "K": d["K"][idx], "V": d["V"][idx], "src_len": d["src_len"][idx]}
+        worst = max(worst, assert_attn_close(out[b0:b0 + len(idx)], oracle_attn(sub), f"large b={b0}.."))
+    say(f"[attn parity] config=large all {cfg.B} sources max_abs_err={worst:.3e}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -175,18 +177,10 @@ PATHS = ("split", "whole1", "whole2", "whole4")
 
 
 def run_path(path, fn):
-    import os
-    old = os.environ.get("FS_ATTN_PATH")
-    os.environ["FS_ATTN_PATH"] = path
-    try:
+    with api.attn_path(path):
         out = fn()
         torch.cuda.synchronize()
         return bits(out)
-    finally:
-        if old is None:
-            del os.environ["FS_ATTN_PATH"]
-        else:
-            os.environ["FS_ATTN_PATH"] = old
 
 
 @pytest.mark.parametrize("dtype,D,k", [("bf16", 64, 4), ("bf16", 64, 5), ("f32", 64, 4), ("bf16", 16, 3),

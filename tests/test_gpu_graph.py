@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 import torch
 
-from paper_2106_04718_amd import api, workloads
+from paper_2106_04718_amd import _native, api, workloads
 
 from _gpu import bits, device, say
 
@@ -127,3 +127,79 @@ def test_record_exchanging_calls_are_refused_under_capture():
     api.beam_select(logits, scores, k, 8, out=sel_out, workspace=sel_ws)
     torch.cuda.synchronize()
     assert torch.isfinite(out.float()).all()
+
+
+def test_fused_step_replays_like_eager_calls():
+    dev = device()
+    B, k, H, S, D, Vsz, t, n = 8, 4, 16, 700, 64, 3000, 60, 3   # 128 rows: one workgroup per row
+    rng = np.random.default_rng(11)
+    q = torch.empty((B, k, H, D), dtype=torch.bfloat16, device=dev)
+    K = torch.empty((B, H, S, D), dtype=torch.bfloat16, device=dev)
+    Vv = torch.empty_like(K)
+    lens = torch.empty(B, dtype=torch.int32, device=dev)
+    tokens = torch.empty((B * k, t), dtype=torch.int32, device=dev)
+    logits = torch.empty((B * k, Vsz), dtype=torch.float32, device=dev)
+    bufs = (q, K, Vv, lens, tokens, logits)
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_cross_attn_workspace_bytes(B, k, H, S, D, torch.bfloat16), dev)
+    fill_inputs(rng, bufs, S, Vsz)
+    api.beam_decode_step(q, K, Vv, lens, tokens, n, logits, out=out, workspace=ws)   # warm-up outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say("[graph] capture of the fused step")
+    with torch.cuda.graph(g):
+        api.beam_decode_step(q, K, Vv, lens, tokens, n, logits, out=out, workspace=ws)
+    for rep in range(4):
+        fill_inputs(rng, bufs, S, Vsz)
+        lg0 = logits.clone()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got_out, got_lg = bits(out), bits(logits)
+        logits.copy_(lg0)
+        eager = api.beam_decode_step(q, K, Vv, lens, tokens, n, logits)
+        torch.cuda.synchronize()
+        assert np.array_equal(got_out, bits(eager)), f"attention, replay {rep}"
+        assert np.array_equal(got_lg, bits(logits)), f"n-gram, replay {rep}"
+
+
+def test_validate_mode_is_refused_under_capture():
+    # Debug mode copies the lengths to the host, which a capturing stream
+    # cannot do: the call is refused before any HIP call and the capture
+    # stays intact.  Outside capture it accepts valid lengths and rejects
+    # an out-of-range one (the kernel never sees it).
+    dev = device()
+    B, k, H, S, D = 8, 4, 16, 300, 64          # 128 rows: the capturable form
+    rng = np.random.default_rng(1)
+    q = draw(rng, (B, k, H, D)).view(torch.bfloat16).to(dev)
+    K = draw(rng, (B, H, S, D)).view(torch.bfloat16).to(dev)
+    Vv = draw(rng, (B, H, S, D)).view(torch.bfloat16).to(dev)
+    lens = torch.from_numpy(rng.integers(1, S + 1, size=B).astype(np.int32)).to(dev)
+    tok = torch.zeros((B * k, 8), dtype=torch.int32, device=dev)
+    logits = torch.zeros((B * k, 50), dtype=torch.float32, device=dev)
+    out = torch.empty_like(q)
+    ws = api.new_workspace(api.beam_cross_attn_workspace_bytes(B, k, H, S, D, torch.bfloat16), dev)
+    say("[graph] debug mode under capture")
+    with api.validate_lengths():
+        api.beam_cross_attn(q, K, Vv, lens, out=out, workspace=ws)    # valid lengths: accepted
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        errs = []
+        with torch.cuda.graph(g):
+            api.ngram_block(tok, 3, logits)
+            for call in (lambda: api.beam_cross_attn(q, K, Vv, lens, out=out, workspace=ws),
+                         lambda: api.beam_decode_step(q, K, Vv, lens, tok, 3, logits, out=out, workspace=ws)):
+                try:
+                    call()
+                except _native.NativeError as e:
+                    errs.append((e.status, str(e)))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert len(errs) == 2, errs
+        assert all(st == _native.FS_ERR_UNSUPPORTED and "FS_VALIDATE" in msg for st, msg in errs), errs
+        bad = lens.clone()
+        bad[3] = S + 1
+        with pytest.raises(_native.NativeError) as ei:
+            api.beam_cross_attn(q, K, Vv, bad, out=out, workspace=ws)
+        assert ei.value.status == _native.FS_ERR_INVALID_ARG and "src_len[3]" in str(ei.value)

@@ -41,23 +41,30 @@ def test_config_parity(name):
 
 
 def test_large_sweep_over_prefix_length():
-    # One [rows, 140] token buffer; step t uses its first t columns (ld = 140).
-    # The first 128 of the 1280 rows keep the sweep quick; rows are independent.
+    # One [1280, 140] token buffer; step t uses its first t columns (ld = 140),
+    # every row at every t.  The changed logits are found on the device (a
+    # bitwise compare against the untouched copy, so any stray write shows)
+    # and must be exactly the oracle's banned (row, token) pairs, set to -inf.
     cfg = workloads.get("large")
     d = workloads.ngram_inputs(cfg)
     rng = np.random.default_rng(99)
-    tokens = workloads.plant_repeats(d["tokens"][:128], cfg.n, cfg.t, rng, per_row=2)
-    logits = np.ascontiguousarray(d["logits"][:128])
-    dev = device()
+    tokens = workloads.plant_repeats(d["tokens"], cfg.n, cfg.t, rng, per_row=2)
     tok = to_dev(tokens)
-    lg0 = to_dev(logits)
-    say("[ngram] large sweep t=1..140")
+    lg0 = to_dev(d["logits"])
+    lg = torch.empty_like(lg0)
+    say(f"[ngram] large sweep t=1..{cfg.t} over {cfg.rows} rows")
+    total = 0
     for t in range(1, cfg.t + 1):
-        want = oracle.ngram_block(tokens, cfg.n, logits, t=t)
-        lg = lg0.clone()
+        want = oracle.ngram_banned(tokens, cfg.n, cfg.V, t=t)
+        lg.copy_(lg0)
         api.ngram_block(tok[:, :t], cfg.n, lg)
-        assert np.array_equal(bits(lg), want.view(np.uint32)), f"t={t}"
-    assert dev.type == "cuda"
+        changed = (lg.view(torch.int32) != lg0.view(torch.int32)).nonzero().cpu().numpy().astype(np.int32)
+        assert np.array_equal(changed.reshape(-1, 2), want), f"t={t}"
+        if len(want):
+            vals = lg[torch.from_numpy(want[:, 0]).long().cuda(), torch.from_numpy(want[:, 1]).long().cuda()]
+            assert bool(torch.isneginf(vals).all()), f"t={t}"
+        total += len(want)
+    assert total > cfg.rows      # planted repeats ban something across the sweep
 
 
 @pytest.mark.parametrize("n", range(1, 11))

@@ -143,20 +143,12 @@ def test_workspace_reused_across_sizes_and_entry_points():
 def test_decompositions_give_identical_bits(dtype, D, k, t):
     # Split-KV with a generated-token record, and the one-workgroup-per-row
     # kernel, fold the same states in the same order: identical bits.
-    import os
     d = case(3, k, 2, 1100, 150, D, dtype, [1100, 0, 513], t, seed=90 + D + t)
     say(f"[prefix paths] dtype={dtype} D={D} k={k} t={t}")
     outs = {}
-    old = os.environ.get("FS_ATTN_PATH")
-    try:
-        for p in ("split", "whole1", "whole2", "whole4"):
-            os.environ["FS_ATTN_PATH"] = p
+    for p in ("split", "whole1", "whole2", "whole4"):
+        with api.attn_path(p):
             outs[p] = bits(run(d))
-    finally:
-        if old is None:
-            os.environ.pop("FS_ATTN_PATH", None)
-        else:
-            os.environ["FS_ATTN_PATH"] = old
     assert np.array_equal(outs["whole1"], outs["split"])
     assert np.array_equal(outs["whole2"], outs["split"])
     assert np.array_equal(outs["whole4"], outs["split"])

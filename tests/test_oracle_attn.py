@@ -205,3 +205,39 @@ def test_rejects_bad_shapes():
     with pytest.raises(ValueError):
         oracle.cross_attn(np.zeros((1, 1, 1, 4)), np.zeros((1, 1, 3, 5)), np.zeros((1, 1, 3, 5)),
                           np.ones(1, np.int32))
+
+
+# ---- the layout of Eq. 1: K/V replicated per beam ---------------------------
+
+@settings(max_examples=40, deadline=None)
+@given(B=st.integers(1, 3), k=st.integers(1, 4), H=st.integers(1, 3), S=st.integers(1, 30),
+       D=st.sampled_from([1, 4, 16]), seed=st.integers(0, 2**31 - 1))
+def test_replicated_layout_matches_library_sdpa_per_hypothesis(B, k, H, S, D, seed):
+    # every hypothesis has its own K/V copy here (they need not be equal)
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((B, k, H, D))
+    K = rng.standard_normal((B * k, H, S, D))
+    V = rng.standard_normal((B * k, H, S, D))
+    lens = rng.integers(-1, S + 2, size=B).astype(np.int32)
+    got = oracle.cross_attn_replicated(q, K, V, lens)
+    want = sdpa_reference(q.reshape(B * k, 1, H, D), K, V, np.repeat(lens, k)).reshape(B, k, H, D)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_replicated_copies_equal_dedup_bitwise():
+    # Eq. 4's claim: with every beam's copy equal to the source's, the
+    # de-duplicated cache gives exactly the replicated result.
+    rng = np.random.default_rng(21)
+    B, k, H, S, D = 3, 5, 2, 41, 16
+    q = rng.standard_normal((B, k, H, D))
+    K = rng.standard_normal((B, H, S, D))
+    V = rng.standard_normal((B, H, S, D))
+    lens = np.array([41, 7, 0], np.int32)
+    rep = oracle.cross_attn_replicated(q, np.repeat(K, k, axis=0), np.repeat(V, k, axis=0), lens)
+    assert np.array_equal(rep, oracle.cross_attn(q, K, V, lens))
+
+
+def test_replicated_rejects_bad_shapes():
+    q = np.zeros((2, 3, 1, 4))
+    with pytest.raises(ValueError):
+        oracle.cross_attn_replicated(q, np.zeros((2, 1, 5, 4)), np.zeros((2, 1, 5, 4)), [5, 5])

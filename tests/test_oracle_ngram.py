@@ -164,3 +164,47 @@ def test_configs_rarely_ban_without_planting():
     out = oracle.ngram_block(d["tokens"], cfg.n, d["logits"])
     per_row = np.isneginf(out).sum() / cfg.rows
     assert per_row < 1.0
+
+
+# ---- the bans as a list of (row, token) pairs ------------------------------
+
+@pytest.mark.parametrize("V,n,tokens,banned,note", HAND, ids=[c[4][:40] for c in HAND])
+def test_banned_pairs_hand_table(V, n, tokens, banned, note):
+    tok = np.array([tokens], dtype=np.int32).reshape(1, len(tokens))
+    pairs = oracle.ngram_banned(tok, n, V)
+    assert [int(r) for r in pairs[:, 0]] == [0] * len(pairs), note
+    assert [int(v) for v in pairs[:, 1]] == sorted(banned), note
+
+
+@settings(max_examples=200, deadline=None)
+@given(
+    V=st.sampled_from([2, 3, 5]),
+    n=st.integers(1, 5),
+    rows=st.lists(st.lists(st.integers(-1, 5), min_size=0, max_size=24), min_size=1, max_size=6),
+)
+def test_banned_pairs_against_brute_force(V, n, rows):
+    t = min(len(r) for r in rows)
+    tok = np.array([r[:t] for r in rows], dtype=np.int32).reshape(len(rows), t)
+    pairs = oracle.ngram_banned(tok, n, V)
+    want = [(r, v) for r in range(len(rows))
+            for v in sorted(brute_force_banned([int(x) for x in tok[r]], n, V))]
+    assert [tuple(int(x) for x in p) for p in pairs] == want
+
+
+def test_banned_pairs_are_the_blocked_positions_with_a_leading_dimension():
+    rng = np.random.default_rng(11)
+    tok = workloads.plant_repeats(rng.integers(0, 9, size=(40, 60)).astype(np.int32), 3, 60, rng, per_row=2)
+    lg = rng.standard_normal((40, 7)).astype(np.float32)
+    for t in (0, 2, 3, 10, 59, 60):
+        out = oracle.ngram_block(tok, 3, lg, t=t)
+        r, v = np.nonzero(np.isneginf(out))
+        pairs = oracle.ngram_banned(tok, 3, 7, t=t)
+        assert np.array_equal(pairs, np.stack([r, v], axis=1).astype(np.int32).reshape(-1, 2))
+
+
+def test_banned_pairs_rejects_invalid_arguments():
+    tok = np.zeros((2, 4), np.int32)
+    with pytest.raises(ValueError):
+        oracle.ngram_banned(tok, 0, 5)
+    with pytest.raises(ValueError):
+        oracle.ngram_banned(tok, 2, 5, t=5)
