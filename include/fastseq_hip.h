@@ -239,6 +239,28 @@ int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32
                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * fs_beam_decode_step for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same step with no workspace argument.  The split-KV
+ * decomposition (fewer than 128 (source, head) rows) keeps its partial
+ * records in an array of FS_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every GPU it runs on until the process ends; the other decompositions use
+ * no scratch.  The call allocates nothing and frees nothing; its first use
+ * on a GPU enqueues a clear of that GPU's array on `stream`.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (other streams, other threads) race and must not be issued.
+ * Arguments, results (bit for bit) and errors are those of
+ * fs_beam_decode_step without the workspace; in addition
+ * FS_ERR_UNSUPPORTED when the split-KV records of these sizes exceed
+ * FS_NOALLOC_SCRATCH_BYTES (see fs_beam_cross_attn_workspace_bytes).
+ */
+#define FS_NOALLOC_SCRATCH_BYTES (8u << 20)
+int fs_beam_decode_step_noalloc(const void *q, const void *K, const void *V, const int32_t *src_len, void *out,
+                                int B, int k, int H, int S, int D, int dtype,
+                                const int32_t *tokens, int ld_tokens, int t, int n, float *logits, int vocab,
+                                void *stream);
+
+/*
  * Tuning controls, for tests and measurements: they replace a size rule of
  * the library for every later call in the process (every thread).  Results
  * do not depend on them except where a call's documentation says so (the

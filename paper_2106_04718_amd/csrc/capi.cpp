@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -140,7 +141,8 @@ int check_attn_sizes(int B, int k, int H, int S, int D, int dtype) {
 // Checks of fs_beam_cross_attn's arguments (also the attention half of the
 // fused decode step); FS_OK or an error with g_last_error set.
 int check_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len, void *out, int B,
-                     int k, int H, int S, int D, int dtype, void *workspace, size_t workspace_bytes) {
+                     int k, int H, int S, int D, int dtype, void *workspace, size_t workspace_bytes,
+                     bool own_scratch = false) {
     const size_t esize = dtype == FS_BF16 ? 2 : 4;
     const size_t q_bytes = (size_t)B * k * H * D * esize;
     const size_t kv_bytes = (size_t)B * H * S * D * esize;
@@ -153,6 +155,7 @@ int check_cross_attn(const void *q, const void *K, const void *V, const int32_t 
     if (overlaps(out, q_bytes, q, q_bytes) || overlaps(out, q_bytes, K, kv_bytes) ||
         overlaps(out, q_bytes, V, kv_bytes) || overlaps(out, q_bytes, src_len, (size_t)B * 4))
         return fail(FS_ERR_INVALID_ARG, "out overlaps an input");
+    if (own_scratch) return FS_OK;   // the library's own array: sized and checked by the caller
     const size_t need = fs::cross_attn_workspace_floats(B, k, H, S, D, (int)esize, false) * sizeof(float);
     if (workspace_bytes < need || (need > 0 && !workspace))
         return fail(FS_ERR_INVALID_ARG, "workspace of %zu bytes at %p; %zu bytes needed",
@@ -251,10 +254,69 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
     return FS_OK;
 }
 
-int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32_t *src_len, void *out,
-                        int B, int k, int H, int S, int D, int dtype,
-                        const int32_t *tokens, int ld_tokens, int t, int n, float *logits, int vocab,
-                        void *workspace, size_t workspace_bytes, void *stream)
+}  // extern "C"
+
+namespace {
+
+// ---- the decode step without a caller workspace ---------------------------
+// The split-KV decomposition keeps its partial records in `scratch`, one
+// file-scope array per GPU, instead of a workspace the caller allocates.  In
+// host code `scratch` only names the symbol: its device address, different
+// on every GPU, comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = FS_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+__global__ void scratch_clear_kernel(uint4 *p, size_t n16) {
+    for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+struct ScratchSlot {
+    void *ptr = nullptr;   // device address of `scratch` on this device
+    bool cleared = false;  // a clear has been enqueued before the first use
+};
+std::mutex g_scratch_mu;
+ScratchSlot g_scratch[kMaxDevices];
+
+// The device address of `scratch` on the device of `s` (the current device
+// for the null stream), found once per device with that device current; the
+// first use on a device enqueues a clear on `s`, so the array starts at zero.
+int scratch_on(hipStream_t s, void **ptr) {
+    int dev = -1;
+    hipError_t e = s ? hipStreamGetDevice(s, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "fs_beam_decode_step_noalloc: device of the stream");
+    if (dev < 0 || dev >= kMaxDevices) return fail(FS_ERR_UNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ScratchSlot &slot = g_scratch[dev];
+    if (!slot.ptr) {
+        int cur = -1;
+        if ((e = hipGetDevice(&cur)) != hipSuccess) return hip_fail(e, "hipGetDevice");
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev) {
+            const hipError_t e2 = hipSetDevice(cur);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e != hipSuccess || !p) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        slot.ptr = p;
+    }
+    if (!slot.cleared) {
+        hipLaunchKernelGGL(scratch_clear_kernel, dim3(256), dim3(256), 0, s, static_cast<uint4 *>(slot.ptr),
+                           kScratchBytes / 16);
+        if ((e = hipGetLastError()) != hipSuccess) return hip_fail(e, "clear of the scratch array");
+        slot.cleared = true;
+    }
+    *ptr = slot.ptr;
+    return FS_OK;
+}
+
+// fs_beam_decode_step, with the caller's workspace (noalloc == false) or the
+// scratch array (noalloc == true, workspace arguments ignored).
+int decode_step(const void *q, const void *K, const void *V, const int32_t *src_len, void *out, int B, int k,
+                int H, int S, int D, int dtype, const int32_t *tokens, int ld_tokens, int t, int n, float *logits,
+                int vocab, void *workspace, size_t workspace_bytes, void *stream, bool noalloc)
 {
     g_last_error.clear();
     int st = check_attn_sizes(B, k, H, S, D, dtype);
@@ -265,7 +327,20 @@ int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32
     const int rows = (int)rows_ll;
     const bool attn = B > 0 && k > 0 && H > 0;
     const bool ngram = rows > 0 && t >= n && vocab > 0;
-    if (attn && (st = check_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype, workspace, workspace_bytes)) != FS_OK)
+    const int esize_i = dtype == FS_BF16 ? 2 : 4;
+    const fs::AttnPath path = attn ? attn_path_for(B * H, S, D, esize_i, false) : fs::AttnPath::kAuto;
+    if (noalloc) {
+        // only the split-KV form keeps records; its need must fit the array
+        const size_t need = path == fs::AttnPath::kSplit
+            ? fs::cross_attn_workspace_floats(B, k, H, S, D, esize_i, false) * sizeof(float) : 0;
+        if (need > kScratchBytes)
+            return fail(FS_ERR_UNSUPPORTED, "fs_beam_decode_step_noalloc: %d rows take the split-KV form, whose "
+                        "%zu bytes of partial records exceed the %zu-byte scratch array", B * H, need, kScratchBytes);
+        workspace = nullptr;
+        workspace_bytes = need;
+    }
+    if (attn && (st = check_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype, noalloc ? nullptr : workspace,
+                                       noalloc ? 0 : workspace_bytes, noalloc)) != FS_OK)
         return st;
     if (ngram) {
         if ((st = check_ngram_buffers(tokens, ld_tokens, rows, t, logits, vocab)) != FS_OK) return st;
@@ -275,7 +350,8 @@ int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32
             const size_t q_bytes = (size_t)B * k * H * D * esize, kv_bytes = (size_t)B * H * S * D * esize;
             const size_t lg_bytes = (size_t)rows * vocab * 4;
             const size_t tok_bytes = ((size_t)(rows - 1) * ld_tokens + t) * 4;
-            const size_t ws_bytes = fs::cross_attn_workspace_floats(B, k, H, S, D, (int)esize, false) * sizeof(float);
+            const size_t ws_bytes = noalloc ? 0
+                : fs::cross_attn_workspace_floats(B, k, H, S, D, (int)esize, false) * sizeof(float);
             if (overlaps(logits, lg_bytes, q, q_bytes) || overlaps(logits, lg_bytes, K, kv_bytes) ||
                 overlaps(logits, lg_bytes, V, kv_bytes) || overlaps(logits, lg_bytes, out, q_bytes) ||
                 overlaps(logits, lg_bytes, src_len, (size_t)B * 4) || overlaps(logits, lg_bytes, workspace, ws_bytes))
@@ -291,18 +367,39 @@ int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32
         if (e != hipSuccess) return hip_fail(e, "fs_beam_decode_step n-gram launch");
         return FS_OK;
     }
-    const int esize = dtype == FS_BF16 ? 2 : 4;
-    const fs::AttnPath path = attn_path_for(B * H, S, D, esize, false);
     if (path == fs::AttnPath::kSplit && capturing(s))
         return fail(FS_ERR_UNSUPPORTED, "fs_beam_decode_step: %d rows take the split-KV form, whose tagged records "
                     "cannot be captured into a graph", B * H);
     if (validate_mode() && (st = validate_lengths(src_len, B, S, s, "src_len")) != FS_OK) return st;
+    if (noalloc && path == fs::AttnPath::kSplit && (st = scratch_on(s, &workspace)) != FS_OK) return st;
     const fs::NgramRows ng{tokens, ld_tokens, rows, t, n, logits, vocab};
     hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
                                          static_cast<float *>(workspace), next_epoch(), s, path,
                                          ngram ? &ng : nullptr);
-    if (e != hipSuccess) return hip_fail(e, "fs_beam_decode_step launch");
+    if (e != hipSuccess) return hip_fail(e, noalloc ? "fs_beam_decode_step_noalloc launch" : "fs_beam_decode_step launch");
     return FS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fs_beam_decode_step(const void *q, const void *K, const void *V, const int32_t *src_len, void *out,
+                        int B, int k, int H, int S, int D, int dtype,
+                        const int32_t *tokens, int ld_tokens, int t, int n, float *logits, int vocab,
+                        void *workspace, size_t workspace_bytes, void *stream)
+{
+    return decode_step(q, K, V, src_len, out, B, k, H, S, D, dtype, tokens, ld_tokens, t, n, logits, vocab,
+                       workspace, workspace_bytes, stream, false);
+}
+
+int fs_beam_decode_step_noalloc(const void *q, const void *K, const void *V, const int32_t *src_len, void *out,
+                                int B, int k, int H, int S, int D, int dtype,
+                                const int32_t *tokens, int ld_tokens, int t, int n, float *logits, int vocab,
+                                void *stream)
+{
+    return decode_step(q, K, V, src_len, out, B, k, H, S, D, dtype, tokens, ld_tokens, t, n, logits, vocab,
+                       nullptr, 0, stream, true);
 }
 
 int fs_set_tuning(int knob, int value)

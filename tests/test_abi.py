@@ -354,3 +354,18 @@ def test_tuning_controls():
     hdr = (ROOT / "include" / "fastseq_hip.h").read_text()
     for name, v in N.ATTN_PATHS.items():
         assert re.search(rf"FS_ATTN_PATH_{name.upper()} = {v}\b", hdr), name
+
+
+def test_noalloc_step_refuses_records_beyond_its_scratch_array():
+    # 127 (source, head) rows take the split-KV form; 64 chunks of records at
+    # k = 8, D = 128 need about 67 MB, more than the library's array
+    lib = N.lib()
+    st = lib.fs_beam_decode_step_noalloc(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, FAKE * 5, 1, 8, 127, 8192, 128,
+                                         N.FS_BF16, FAKE * 6, 8, 8, 3, FAKE * 7, 100, None)
+    assert st == N.FS_ERR_UNSUPPORTED and "scratch array" in N.last_error()
+    # argument errors are those of fs_beam_decode_step
+    st = lib.fs_beam_decode_step_noalloc(None, FAKE * 2, FAKE * 3, FAKE * 4, FAKE * 5, 2, 4, 2, 64, 16,
+                                         N.FS_F32, FAKE * 6, 8, 8, 3, FAKE * 7, 100, None)
+    assert st == N.FS_ERR_INVALID_ARG and "null" in N.last_error()
+    hdr = (ROOT / "include" / "fastseq_hip.h").read_text()
+    assert re.search(r"#define FS_NOALLOC_SCRATCH_BYTES \(8u << 20\)", hdr)
