@@ -93,7 +93,7 @@ const char *fs_last_error(void);
 
 /*
  * Workspace, in bytes, that fs_beam_cross_attn needs for these sizes
- * (per-chunk softmax partials, fp32 values tagged with the call).  Zero-fill
+ * (per-tile softmax partials, fp32 values tagged with the call).  Zero-fill
  * it before its first use.  0 for empty problems; (size_t)-1 for
  * invalid or unsupported sizes.  The size depends on every argument, so
  * query it again whenever one changes.
@@ -119,7 +119,7 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  *   out      [B, k, H, D]  dtype    result, rounded to nearest-even from fp32
  *   workspace, workspace_bytes      scratch of at least
  *            fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype)
- *            bytes (per-chunk partials).  It must be zero-filled once
+ *            bytes (per-tile partials).  It must be zero-filled once
  *            before its first use and not written by anything else after
  *            that: each call marks the words it writes with a tag of its
  *            own, and an all-zero or earlier-tagged word is never taken as

@@ -743,13 +743,15 @@ struct WaveLds {
 // and the output becomes NaN if it never does (a loud failure instead of a
 // silent wrong merge or an endless wait).
 //
-// With a generated-token segment (SPLIT), record slot NC of (b, h) holds the
-// per-beam state of that segment; it is merged after the prefix chunks, and
+// The records are the row's tile states, one per tile of keys in key order
+// (record slot j holds tile j), folded one by one from the empty state.
+// With a generated-token segment (SPLIT), record slot NT of (b, h) holds the
+// per-beam state of that segment; it is merged after the prefix tiles, and
 // the merger also writes the rows whose prefix has at most one chunk.
 template <int D, bool BF16, int KB, bool SPLIT>
 __device__ __forceinline__ void merge_chunks(const unsigned long long *__restrict__ part,
                                              const int32_t *__restrict__ src_len, void *__restrict__ out,
-                                             int bh, int n_bh, int H, int S, int NC, int t,
+                                             int bh, int n_bh, int H, int S, int NT, int t,
                                              unsigned long long epoch)
 {
     using G = Geo<D, BF16>;
@@ -757,12 +759,12 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
     const int b = bh / H;
     const int h = bh - b * H;
     const int L = min(max(src_len[b], 0), S);
-    const int nc = (L + G::kChunk - 1) / G::kChunk;
-    if (!SPLIT && nc <= 1) return;  // written by the chunk workgroup itself
-    const int nrec = nc + (SPLIT && t > 0 ? 1 : 0);  // records to merge, in order
+    if (!SPLIT && (L + G::kChunk - 1) / G::kChunk <= 1) return;  // written by the chunk workgroup itself
+    const int nc = (L + G::kTile - 1) / G::kTile;             // tile records of the prefix, in key order
+    const int nrec = nc + (SPLIT && t > 0 ? 1 : 0);          // records to merge, in order
     constexpr int kRec = KB * (D + 2);
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
-    const unsigned long long *recs = part + (size_t)bh * (NC + (SPLIT ? 1 : 0)) * kRec;
+    const unsigned long long *recs = part + (size_t)bh * (NT + (SPLIT ? 1 : 0)) * kRec;
     const size_t obase = ((size_t)b * KB * H + h) * D;
     constexpr int kBatch = 4;  // records whose words are loaded together
     for (int x = threadIdx.x; x < KB * D; x += kBlock) {
@@ -774,8 +776,8 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
             unsigned long long wv[kBatch][3];
 #pragma unroll
             for (int q2 = 0; q2 < kBatch; ++q2) {
-                // the generated-token record sits in slot NC
-                const int slot = (SPLIT && c0 + q2 == nc) ? NC : c0 + q2;
+                // the generated-token record sits in slot NT
+                const int slot = (SPLIT && c0 + q2 == nc) ? NT : c0 + q2;
 #pragma unroll
                 for (int f = 0; f < 3; ++f) {
                     wv[q2][f] = tag;
@@ -787,7 +789,7 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
 #pragma unroll
             for (int q2 = 0; q2 < kBatch; ++q2) {
                 if (c0 + q2 >= nrec) break;
-                const int slot = (SPLIT && c0 + q2 == nc) ? NC : c0 + q2;
+                const int slot = (SPLIT && c0 + q2 == nc) ? NT : c0 + q2;
 #pragma unroll
                 for (int f = 0; f < 3; ++f) {
                     const unsigned long long *a = recs + (size_t)slot * kRec + at[f];
@@ -892,7 +894,7 @@ __device__ __forceinline__ void generated_state(const uint4 *__restrict__ q, con
 template <int D, bool BF16, int KB, bool ANC>
 __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                  const uint4 *__restrict__ Vt, unsigned long long *__restrict__ part,
-                                                 int bh, int n_bh, int H, int NC, int T, int t,
+                                                 int bh, int n_bh, int H, int NT, int T, int t,
                                                  float scale_log2, unsigned long long epoch, void *lds,
                                                  const int32_t *__restrict__ anc, int ld_anc)
 {
@@ -903,7 +905,7 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     const int w = wave_id();
     constexpr int kRec = KB * (D + 2);
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
-    unsigned long long *rec = part + ((size_t)bh * (NC + 1) + NC) * kRec;
+    unsigned long long *rec = part + ((size_t)bh * (NT + 1) + NT) * kRec;
     for (int i = w; i < KB; i += kWaves) {
         GenState<D> gs;
         const size_t hyp = (size_t)b * KB + i;
@@ -956,7 +958,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     int g = blockIdx.x - ngj.blocks;
     if constexpr (SPLIT) {
         if (g < n_bh8) {
-            attend_generated<D, BF16, KB, ANC>(q, Kt, Vt, part, g, n_bh, H, NC, T, t, scale_log2, epoch,
+            attend_generated<D, BF16, KB, ANC>(q, Kt, Vt, part, g, n_bh, H, NC * kWaves, T, t, scale_log2, epoch,
                                           &t_lds[wave_id()][0], anc, ld_anc);
             return;
         }
@@ -964,7 +966,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     }
     const int n_chunk_blocks = n_bh8 * NC;
     if (g >= n_chunk_blocks) {
-        merge_chunks<D, BF16, KB, SPLIT>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC, t, epoch);
+        merge_chunks<D, BF16, KB, SPLIT>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC * kWaves, t, epoch);
         return;
     }
     const int xcd = g % kXcds;
@@ -1004,30 +1006,32 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     __syncthreads();
 
     if (!SPLIT && nc == 1) {
+        // the whole row: its tile states folded in key order from the empty state
         for (int x = tid; x < KB * D; x += kBlock) {
             const int i = x / D, d = x - i * D;
-            float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * TL::kAStride + d];
+            float mm = -INFINITY, ll = 0.f, aa = 0.f;
 #pragma unroll
-            for (int ww = 1; ww < kWaves; ++ww)
+            for (int ww = 0; ww < kWaves; ++ww)
                 merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * TL::kAStride + d]);
             store_out<BF16>(out, obase + (size_t)i * H * D + d, aa / ll);
         }
         return;
     }
 
-    // Partial record of (b, h, c): acc[KB][D], then m[KB], then l[KB].
-    unsigned long long *rec = part + ((size_t)bh * (NC + (SPLIT ? 1 : 0)) + c) * (KB * (D + 2));
+    // One record per tile of the chunk (slot = tile index in the row):
+    // acc[KB][D], then m[KB], then l[KB].
+    const int NT = NC * kWaves;
+    const int ntile = min(kWaves, (j1 - j0 + kTile - 1) / kTile);   // tiles of this chunk that hold keys
     const unsigned long long tag = (epoch & 0xffffffffull) << 32;
-    for (int x = tid; x < KB * D; x += kBlock) {
-        const int i = x / D, d = x - i * D;
-        float mm = m_lds[0][i], ll = l_lds[0][i], aa = a_lds(0)[i * TL::kAStride + d];
-#pragma unroll
-        for (int ww = 1; ww < kWaves; ++ww)
-            merge_state(mm, ll, aa, m_lds[ww][i], l_lds[ww][i], a_lds(ww)[i * TL::kAStride + d]);
-        store_word(rec + x, tag, aa);
-        if (d == 0) {
-            store_word(rec + KB * D + i, tag, mm);
-            store_word(rec + KB * D + KB + i, tag, ll);
+    for (int ww = 0; ww < ntile; ++ww) {
+        unsigned long long *rec = part + ((size_t)bh * (NT + (SPLIT ? 1 : 0)) + c * kWaves + ww) * (KB * (D + 2));
+        for (int x = tid; x < KB * D; x += kBlock) {
+            const int i = x / D, d = x - i * D;
+            store_word(rec + x, tag, a_lds(ww)[i * TL::kAStride + d]);
+            if (d == 0) {
+                store_word(rec + KB * D + i, tag, m_lds[ww][i]);
+                store_word(rec + KB * D + KB + i, tag, l_lds[ww][i]);
+            }
         }
     }
 }
@@ -1161,15 +1165,14 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
                 const int i = x / D, d = x - i * D;
                 for (int g = 0; g < P && j0 + g < njobs; ++g) {
                     if (j0 + g < ng) continue;  // the generated-token job is folded last
-                    const int w0 = g * kWaves;
-                    const float *a0 = reinterpret_cast<const float *>(&t_lds[w0][0]);
-                    float mm = m_lds[w0][i], ll = l_lds[w0][i], aa = a0[i * TL::kAStride + d];
+                    // the chunk's tile states, in key order (a tile past the
+                    // row's end holds the empty state, which folds to nothing)
 #pragma unroll
-                    for (int ww = 1; ww < kWaves; ++ww) {
-                        const float *aw = reinterpret_cast<const float *>(&t_lds[w0 + ww][0]);
-                        merge_state(mm, ll, aa, m_lds[w0 + ww][i], l_lds[w0 + ww][i], aw[i * TL::kAStride + d]);
+                    for (int ww = 0; ww < kWaves; ++ww) {
+                        const int w0 = g * kWaves + ww;
+                        const float *aw = reinterpret_cast<const float *>(&t_lds[w0][0]);
+                        merge_state(Rm[p], Rl[p], Ra[p], m_lds[w0][i], l_lds[w0][i], aw[i * TL::kAStride + d]);
                     }
-                    merge_state(Rm[p], Rl[p], Ra[p], mm, ll, aa);
                 }
             }
         }
@@ -1344,9 +1347,11 @@ int cross_attn_chunk_keys(int D, int esize) {
 
 size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize, bool split) {
     const int C = cross_attn_chunk_keys(D, esize);
-    const size_t NC = (size_t)std::max(1, (S + C - 1) / C) + (split ? 1 : 0);
+    // one record per tile of the row (kWaves tiles per chunk), plus the
+    // generated-token record of the split cache
+    const size_t NT = (size_t)std::max(1, (S + C - 1) / C) * kWaves + (split ? 1 : 0);
     const size_t n_bh = (size_t)B * H;
-    const size_t part = n_bh * NC * (size_t)k * (size_t)(D + 2);
+    const size_t part = n_bh * NT * (size_t)k * (size_t)(D + 2);
     return 2 * part;  // 64-bit partial-record words
 }
 

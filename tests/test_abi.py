@@ -91,12 +91,13 @@ def test_cross_attn_empty_problems_return_ok_without_launch():
 def test_workspace_bytes():
     f = N.lib().fs_beam_cross_attn_workspace_bytes
     assert f(0, 4, 16, 1024, 64, N.FS_BF16) == 0
-    assert 0 < f(2, 4, 2, 0, 16, N.FS_F32) < 4096                 # S = 0: one empty chunk column
+    assert f(2, 4, 2, 0, 16, N.FS_F32) == 2 * 2 * 4 * 4 * 18 * 8   # S = 0: one empty chunk column of 4 tiles
     assert f(2, 4, 2, 64, 48, N.FS_F32) == 2**64 - 1
     assert f(-1, 4, 2, 64, 16, N.FS_F32) == 2**64 - 1
-    # per (b, h, 256-key chunk): k * (D + 2) 8-byte tagged partials
+    # per (b, h, 64-key tile): k * (D + 2) 8-byte tagged partials (tiles of
+    # four 256-key chunks at D = 64, bf16)
     a = f(32, 4, 16, 1024, 64, N.FS_BF16)
-    assert a == 32 * 16 * 4 * 4 * 66 * 8
+    assert a == 32 * 16 * 16 * 4 * 66 * 8
     assert f(64, 4, 16, 1024, 64, N.FS_BF16) == 2 * a
     assert f(32, 4, 16, 1025, 64, N.FS_BF16) > a
     assert f(32, 4, 16, 1023, 64, N.FS_BF16) == a
