@@ -26,6 +26,9 @@
  *                       the same maintenance without moving rows: an ancestry
  *                       table of the generated tokens, and the split-cache
  *                       attention that reads its generated rows through it.
+ *   fs_postproc_*       asynchronous post-processing (Section 4.3): a host
+ *                       thread detokenises finished hypotheses while the GPU
+ *                       generates the next batch.
  *
  * Conventions shared by every entry point
  *   - Pointers named "device" are HIP device memory; the caller owns every
@@ -425,6 +428,54 @@ int fs_beam_prefix_attn_indirect(const void *q, const void *Kp, const void *Vp, 
                                  const void *Kt, const void *Vt, const int32_t *anc, int ld_anc, int T, int t,
                                  void *out, int B, int k, int H, int N, int D, int dtype, void *workspace,
                                  size_t workspace_bytes, void *stream);
+
+/*
+ * Asynchronous post-processing of finished hypotheses (Section 4.3): a host
+ * thread detokenises and writes out batch i while the GPU generates batch
+ * i + 1.  A handle owns `slots` staging buffers of pinned host memory of
+ * max_rows x max_len ids each (hipHostMalloc), one event per slot and the
+ * worker thread; it is the only part of the library that allocates, and it
+ * does so in fs_postproc_create only.
+ *
+ * Detokenisation is byte-level: token v is the UTF-8 text
+ * vocab[offsets[v] .. offsets[v+1]) over an alphabet of one symbol per byte
+ * -- a printable byte (0x21-0x7E, 0xA1-0xAC, 0xAE-0xFF) stands for itself,
+ * the other bytes in increasing order are the code points 0x100, 0x101, ...
+ * -- and the output bytes are recovered symbol by symbol (other characters
+ * are dropped).  Each row becomes one line: the bytes of its ids up to its
+ * first `eos` id (or its length), then '\n'; ids outside [0, V) are skipped.
+ * Batches are written in submission order, rows in order.
+ *
+ *   fs_postproc_create   copies the vocabulary, opens `path` for writing (NULL:
+ *                        keep the bytes in memory), allocates the staging and
+ *                        starts the worker.  *out receives the handle.
+ *   fs_postproc_submit   tokens [rows, ld] int32 in device memory (columns
+ *                        0..t-1): enqueues their copy into the next staging
+ *                        buffer on `stream` (after the work already on it)
+ *                        and an event, hands the batch to the worker and
+ *                        returns; it waits only while that buffer's previous
+ *                        batch is not written yet.  One submitting thread.
+ *   fs_postproc_flush    waits until every submitted batch is written (and
+ *                        the file flushed); reports the first worker error.
+ *   fs_postproc_output   between a flush and the next submit: the bytes kept
+ *                        in memory -- copies at most cap of them into buf and
+ *                        returns their total size.
+ *   fs_postproc_busy_seconds  host time the worker has spent detokenising and
+ *                        writing (not waiting).
+ *   fs_postproc_destroy  finishes the submitted batches, stops the worker and
+ *                        frees the handle.
+ * Errors: FS_ERR_INVALID_ARG for null pointers, sizes below 1 or above the
+ * staging, decreasing offsets or an unopenable path; FS_ERR_UNSUPPORTED for
+ * staging above 2^31 ids; FS_ERR_HIP for a failed allocation, copy or event.
+ */
+typedef struct fs_postproc fs_postproc;
+int fs_postproc_create(fs_postproc **out, const char *vocab, const int64_t *offsets, int V, int eos, int max_rows,
+                       int max_len, int slots, const char *path);
+int fs_postproc_submit(fs_postproc *pp, const int32_t *tokens, int ld, int rows, int t, void *stream);
+int fs_postproc_flush(fs_postproc *pp);
+size_t fs_postproc_output(fs_postproc *pp, char *buf, size_t cap);
+double fs_postproc_busy_seconds(fs_postproc *pp);
+void fs_postproc_destroy(fs_postproc *pp);
 
 #ifdef __cplusplus
 }

@@ -22,6 +22,9 @@ module only marshals numpy arrays into it:
 * :func:`cache_reorder` -- the per-beam cache reorder after a selection step
   (Section 2.2 cache maintenance, Section 4.1.1): each new hypothesis takes
   its parent's generated-token cache.
+* :func:`detokenize` -- the post-processing of finished hypotheses
+  (Section 4.3): byte-level detokenisation of each row up to its
+  end-of-sequence id, one line per row.
 * :func:`ancestry_step` and :func:`prefix_attn_indirect` -- the same
   maintenance without moving rows: a table of which beam's row holds each
   generated token, and the split-cache attention read through it.
@@ -338,3 +341,40 @@ def prefix_attn_indirect(q, Kp, Vp, prefix_len, Kt, Vt, anc, t: int) -> np.ndarr
     ancestry table (definition: gather the rows, then :func:`prefix_attn`)."""
     k = np.asarray(q).shape[1]
     return prefix_attn(q, Kp, Vp, prefix_len, gather_generated(Kt, anc, k, t), gather_generated(Vt, anc, k, t), t)
+
+
+def _symbol_bytes() -> dict:
+    """Code point -> byte of the byte-level alphabet: a printable byte
+    (0x21-0x7E, 0xA1-0xAC, 0xAE-0xFF) is its own symbol, the remaining
+    bytes in increasing order are the code points 0x100, 0x101, ..."""
+    table, nxt = {}, 0x100
+    for b in range(256):
+        if 0x21 <= b <= 0x7E or 0xA1 <= b <= 0xAC or 0xAE <= b <= 0xFF:
+            table[b] = b
+        else:
+            table[nxt] = b
+            nxt += 1
+    return table
+
+
+def detokenize(tokens, vocab: list, eos: int) -> bytes:
+    """Post-processing of finished hypotheses (Section 4.3), synchronously:
+    each row of ``tokens`` [rows, t] becomes one line -- the bytes of its
+    tokens up to its first ``eos`` id, then a newline.  A token is the
+    symbol string ``vocab[id]``; each symbol of the byte alphabet gives back
+    its byte, other characters give nothing, and ids outside the vocabulary
+    are skipped."""
+    table = _symbol_bytes()
+    out = bytearray()
+    for row in np.asarray(tokens):
+        for v in row:
+            v = int(v)
+            if v == eos:
+                break
+            if 0 <= v < len(vocab):
+                for ch in vocab[v]:
+                    b = table.get(ord(ch))
+                    if b is not None:
+                        out.append(b)
+        out.append(0x0A)
+    return bytes(out)

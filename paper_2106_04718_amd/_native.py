@@ -50,6 +50,13 @@ SIGNATURES = [
     ("fs_beam_ancestry_step", _c_int, [_vp, _c_int, _vp] + [_c_int] * 3 + [_vp]),
     ("fs_beam_prefix_attn_indirect", _c_int,
      [_vp] * 7 + [_c_int] * 3 + [_vp] + [_c_int] * 6 + [_vp, _c_size, _vp]),
+    ("fs_postproc_create", _c_int,
+     [ctypes.POINTER(_vp), ctypes.c_char_p, _vp] + [_c_int] * 5 + [ctypes.c_char_p]),
+    ("fs_postproc_submit", _c_int, [_vp, _vp, _c_int, _c_int, _c_int, _vp]),
+    ("fs_postproc_flush", _c_int, [_vp]),
+    ("fs_postproc_output", _c_size, [_vp, _vp, _c_size]),
+    ("fs_postproc_busy_seconds", ctypes.c_double, [_vp]),
+    ("fs_postproc_destroy", None, [_vp]),
 ]
 
 _lib = None
@@ -101,6 +108,12 @@ def status_string(status: int) -> str:
 
 def last_error() -> str:
     return lib().fs_last_error().decode()
+
+
+def check_lib(status: int) -> None:
+    """Raise on a non-OK status of a call made through lib()."""
+    if status != FS_OK:
+        raise NativeError(status, last_error())
 
 
 def check(status: int) -> None:

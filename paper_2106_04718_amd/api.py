@@ -438,3 +438,78 @@ def cache_reorder(K: torch.Tensor, V: torch.Tensor | None, parent: torch.Tensor,
     with _on(dev):
         _N.check(_N.ext().fs_cache_reorder(K.data_ptr(), 0 if V is None else V.data_ptr(), parent.data_ptr(),
                                            rows // k, int(k), H, T, tp, D, _DTYPES[K.dtype], _stream_ptr(dev)))
+
+
+class PostProcessor:
+    """Asynchronous post-processing of finished hypotheses (Section 4.3).
+
+    A host thread of the library turns the token ids of a finished batch
+    into text -- byte-level detokenisation, one line per row up to its
+    end-of-sequence id -- and writes it to ``path`` (or keeps it in memory),
+    while the GPU goes on with the next batch.  ``vocab`` holds the token
+    strings over the byte alphabet (see include/fastseq_hip.h).  The handle
+    owns ``slots`` pinned staging buffers of ``max_rows`` x ``max_len`` ids.
+    """
+
+    def __init__(self, vocab: list, eos: int, max_rows: int, max_len: int, slots: int = 2,
+                 path: str | None = None):
+        import ctypes
+        import numpy as np
+        enc = [s.encode("utf-8") for s in vocab]
+        off = np.zeros(len(enc) + 1, np.int64)
+        off[1:] = np.cumsum([len(e) for e in enc])
+        data = b"".join(enc) or b"\0"
+        self._lib = _N.lib()
+        self._h = ctypes.c_void_p()
+        _N.check_lib(self._lib.fs_postproc_create(
+            ctypes.byref(self._h), data, off.ctypes.data, len(vocab), int(eos), int(max_rows), int(max_len),
+            int(slots), None if path is None else str(path).encode()))
+
+    def submit(self, tokens: torch.Tensor, t: int | None = None) -> None:
+        """Hand over a finished batch: tokens [rows, ld] int32 on the GPU
+        (the first ``t`` columns, default all), after the work already on
+        torch's current stream.  Returns at once unless every staging
+        buffer is still being written."""
+        if not isinstance(tokens, torch.Tensor) or tokens.device.type != "cuda" or tokens.dtype != torch.int32:
+            raise ValueError("tokens must be an int32 GPU tensor")
+        if tokens.dim() != 2 or (tokens.shape[1] > 1 and tokens.stride(1) != 1):
+            raise ValueError("tokens must be [rows, ld] with unit column stride")
+        rows, cols = tokens.shape
+        t = cols if t is None else int(t)
+        ld = tokens.stride(0) if rows > 1 else cols
+        with _on(tokens.device):
+            _N.check_lib(self._lib.fs_postproc_submit(self._h, tokens.data_ptr(), ld, rows, t,
+                                                      _stream_ptr(tokens.device)))
+
+    def flush(self) -> None:
+        """Wait until every submitted batch is written."""
+        _N.check_lib(self._lib.fs_postproc_flush(self._h))
+
+    def output(self) -> bytes:
+        """The text kept in memory (after a flush)."""
+        import ctypes
+        n = self._lib.fs_postproc_output(self._h, None, 0)
+        buf = ctypes.create_string_buffer(max(1, n))
+        self._lib.fs_postproc_output(self._h, buf, n)
+        return buf.raw[:n]
+
+    def busy_seconds(self) -> float:
+        """Host time the worker has spent detokenising and writing."""
+        return float(self._lib.fs_postproc_busy_seconds(self._h))
+
+    def close(self) -> None:
+        if self._h:
+            self._lib.fs_postproc_destroy(self._h)
+            self._h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # noqa: BLE001 - interpreter shutdown
+            pass

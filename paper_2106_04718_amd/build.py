@@ -19,7 +19,7 @@ CSRC = PKG / "csrc"
 BUILD = PKG / "_build"
 LIB = PKG / "libfastseq_hip.so"
 EXT = PKG / ("_fastseq_ext" + sysconfig.get_config_var("EXT_SUFFIX"))
-SOURCES = ["capi.cpp", "cross_attn.hip", "ngram_block.hip", "beam_select.hip", "cache_reorder.hip"]  # pyext.c is built by build_ext
+SOURCES = ["capi.cpp", "cross_attn.hip", "ngram_block.hip", "beam_select.hip", "cache_reorder.hip", "postproc.cpp"]  # pyext.c is built by build_ext
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

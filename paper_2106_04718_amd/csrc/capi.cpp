@@ -32,6 +32,15 @@ int fail(int status, const char *fmt, ...) {
     return status;
 }
 
+}  // namespace
+
+int fs::set_error(int status, const char *msg) {
+    g_last_error = msg;
+    return status;
+}
+
+namespace {
+
 int hip_fail(hipError_t e, const char *what) {
     return fail(FS_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }

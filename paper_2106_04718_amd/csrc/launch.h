@@ -9,6 +9,10 @@
 
 namespace fs {
 
+// Records `msg` as the calling thread's fs_last_error() and returns `status`
+// (the C ABI's error slot, shared by every entry point).
+int set_error(int status, const char *msg);
+
 // Keys per split-KV chunk of the cross-attention.  It depends only on the
 // row size (D and element size), never on B, k or the lengths, so the
 // reduction order -- and hence every output bit -- is the same whether a

@@ -329,3 +329,62 @@ def ancestry_inputs(cfg) -> dict:
     prng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, cfg.index, 3001]))
     parent = np.floor(cfg.k * prng.random(rows) ** 2).astype(np.int32)
     return {"anc": anc, "parent": parent}
+
+
+# ---- post-processing workload (Section 4.3) ---------------------------------
+#
+# A synthetic byte-level vocabulary in the form byte-level BPE vocabularies
+# take: every byte is written as one symbol (a printable byte as itself, the
+# others -- in increasing order -- as the code points 0x100, 0x101, ...), and
+# a token is the symbol string of a few bytes of text-like content.  The last
+# id is the end-of-sequence token.
+
+def _byte_symbol(b: int) -> str:
+    printable = 0x21 <= b <= 0x7E or 0xA1 <= b <= 0xAC or 0xAE <= b <= 0xFF
+    if printable:
+        return chr(b)
+    others = [x for x in range(256) if not (0x21 <= x <= 0x7E or 0xA1 <= x <= 0xAC or 0xAE <= x <= 0xFF)]
+    return chr(0x100 + others.index(b))
+
+
+_SYMBOLS = [_byte_symbol(b) for b in range(256)]
+
+
+def byte_vocab(V: int, seed: int = 0) -> list:
+    """V token strings over the byte alphabet; id V-1 is '</s>'."""
+    rng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, 4300, seed]))
+    letters = np.frombuffer(b"etaoinshrdlucmfwypvbgkjqxz", np.uint8)
+    punct = np.frombuffer(b".,;:'\"!?-()0123456789", np.uint8)
+    vocab = []
+    for _ in range(V - 1):
+        n = int(min(12, 1 + rng.poisson(3)))
+        kind = rng.random(n)
+        raw = np.where(kind < 0.72, letters[rng.integers(0, len(letters), n)],
+                       np.where(kind < 0.87, 0x20,
+                                np.where(kind < 0.96, punct[rng.integers(0, len(punct), n)],
+                                         rng.integers(0x80, 0x100, n))))
+        vocab.append("".join(_SYMBOLS[int(b)] for b in raw))
+    vocab.append("</s>")
+    return vocab
+
+
+def vocab_utf8(vocab: list):
+    """The vocabulary as one UTF-8 byte string and int64 offsets [V+1]."""
+    enc = [s.encode("utf-8") for s in vocab]
+    off = np.zeros(len(enc) + 1, np.int64)
+    off[1:] = np.cumsum([len(e) for e in enc])
+    return b"".join(enc), off
+
+
+def finished_batches(cfg, batches: int, seed: int = 0) -> np.ndarray:
+    """Token ids of `batches` batches of finished hypotheses [batches, rows, t]
+    (Zipf ids over the vocabulary, each row ended by the end-of-sequence id
+    V-1 at a uniform position in its second half)."""
+    rng = np.random.default_rng(np.random.SeedSequence([SEED_BASE, 4301, cfg.index, seed]))
+    tok = zipf_tokens(rng, (batches, cfg.rows, cfg.t), cfg.V - 1, cfg.zipf_s if cfg.token_dist == "zipf" else 1.1)
+    ends = rng.integers(cfg.t // 2, cfg.t + 1, size=(batches, cfg.rows))
+    for bi in range(batches):
+        for r in range(cfg.rows):
+            if ends[bi, r] < cfg.t:
+                tok[bi, r, ends[bi, r]] = cfg.V - 1
+    return np.ascontiguousarray(tok.astype(np.int32))

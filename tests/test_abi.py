@@ -370,3 +370,29 @@ def test_noalloc_step_refuses_records_beyond_its_scratch_array():
     assert st == N.FS_ERR_INVALID_ARG and "null" in N.last_error()
     hdr = (ROOT / "include" / "fastseq_hip.h").read_text()
     assert re.search(r"#define FS_NOALLOC_SCRATCH_BYTES \(8u << 20\)", hdr)
+
+
+def test_postproc_rejects_bad_arguments_before_any_hip_call():
+    import ctypes
+    import numpy as np
+    lib = N.lib()
+    h = ctypes.c_void_p()
+    off = np.array([0, 1, 3], np.int64)
+    data = b"abc"
+    assert lib.fs_postproc_create(None, data, off.ctypes.data, 2, 1, 4, 4, 2, None) == N.FS_ERR_INVALID_ARG
+    assert lib.fs_postproc_create(ctypes.byref(h), data, off.ctypes.data, 0, 1, 4, 4, 2, None) == N.FS_ERR_INVALID_ARG
+    assert "vocabulary" in N.last_error()
+    assert lib.fs_postproc_create(ctypes.byref(h), data, off.ctypes.data, 2, 1, 0, 4, 2, None) == N.FS_ERR_INVALID_ARG
+    assert lib.fs_postproc_create(ctypes.byref(h), data, off.ctypes.data, 2, 1, 4, 4, 0, None) == N.FS_ERR_INVALID_ARG
+    bad = np.array([0, 2, 1], np.int64)
+    assert lib.fs_postproc_create(ctypes.byref(h), data, bad.ctypes.data, 2, 1, 4, 4, 2, None) == N.FS_ERR_INVALID_ARG
+    assert "decrease" in N.last_error()
+    assert lib.fs_postproc_create(ctypes.byref(h), data, off.ctypes.data, 2, 1, 1 << 16, 1 << 16, 2, None) \
+        == N.FS_ERR_UNSUPPORTED
+    assert lib.fs_postproc_create(ctypes.byref(h), data, off.ctypes.data, 2, 1, 4, 4, 2,
+                                  b"/nonexistent-dir/out.txt") == N.FS_ERR_INVALID_ARG
+    assert h.value is None
+    assert lib.fs_postproc_submit(None, FAKE, 4, 2, 4, None) == N.FS_ERR_INVALID_ARG
+    assert lib.fs_postproc_flush(None) == N.FS_ERR_INVALID_ARG
+    assert lib.fs_postproc_output(None, None, 0) == 0
+    lib.fs_postproc_destroy(None)
