@@ -15,14 +15,15 @@
 //   * one workgroup per (row, slice of the vocabulary): it issues all its
 //     row loads first (16 bytes per lane and load), scans the row's history
 //     for banned tokens into an LDS bitmap while they are in flight, then
-//     takes each wave's (max, sum of exp) in two passes over registers.  Its
-//     c best candidates come from a threshold: in each wave, the minimum over
-//     G >= c lane blocks of the block maxima has at least G positions above
-//     it, so the c best of the slice all lie at or above the largest of these
-//     bounds; the few positions there are collected in LDS by ballots and
-//     ranked.  A slice with too many positions at the threshold (equal
-//     logits) takes an exact c-round selection instead.  The results go to
-//     the workspace as tagged partial records;
+//     takes each wave's (max, sum of exp) in two passes over registers, then
+//     sets its banned values to -inf.  Its c best candidates come from a
+//     threshold: the c-th largest of 64 block maxima (blocks of adjacent
+//     lanes) has c distinct positions at or above it, so the c best of the
+//     slice all lie there.  The few positions at or above it (about c for
+//     random logits) are collected in LDS by ballots and ranked.  A slice
+//     with too many positions at the threshold (equal logits) takes an exact
+//     c-round selection instead.  The results go to the workspace as tagged
+//     partial records;
 //   * one merger workgroup per source, after all slice workgroups in the
 //     grid, combines the slices' (max, sum) into each row's lse, scores the
 //     k * slices * c candidates and keeps the c best.
@@ -55,6 +56,8 @@ constexpr int kMergeCap = 1024;          // candidates a merger ranks: k * slice
 constexpr int kMergeWords = 8 * kThreads; // record words a merger reads: k * slices * (2 + 2c)
 constexpr int kMaxSpins = 1 << 14;       // bounded re-reads of a record word (about 10 ms)
 constexpr int kNMax = 8;                 // n-gram sizes whose first window is loaded ahead
+constexpr int kWaves = kThreads / kWave;
+constexpr int kBlocks = kWave / kWaves;   // threshold blocks per wave: 64 in a workgroup
 
 // Order-preserving 32-bit image of a float (larger value, larger image);
 // -0 is taken as +0.
@@ -193,27 +196,35 @@ __device__ __forceinline__ void lds_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// Lower bound of the G-th largest of the wave's 64 lane values, G = 1 << lg:
-// the minimum over G blocks of 64/G adjacent lanes of each block's maximum.
-// The G block maxima sit in distinct lanes, so at least G lanes hold a value
-// at or above the result.  The first 6 - lg butterfly steps take maxima
-// inside the blocks, the rest minima across them; every lane ends with the
-// same value.
+// Maximum over each block of kWaves adjacent lanes (the first log2(kWaves)
+// butterfly steps); every lane of a block ends with its block's maximum.
 template <int STEP = 0>
-__device__ __forceinline__ float block_max_min(float x, int lg) {
-    if constexpr (STEP == 6) {
+__device__ __forceinline__ float block_max(float x) {
+    if constexpr ((1 << STEP) >= kWaves) {
         return x;
     } else {
         uint32_t p, unused;
         partner<STEP>(p, unused, __float_as_uint(x), 0u);
-        const float o = __uint_as_float(p);
-        return block_max_min<STEP + 1>(STEP < 6 - lg ? fmaxf(x, o) : fminf(x, o), lg);
+        return block_max<STEP + 1>(fmaxf(x, __uint_as_float(p)));
     }
+}
+
+// The c-th largest of the wave's 64 lane values, counted with multiplicity
+// (1 <= c <= 64; no value is NaN): c rounds, each taking the wave maximum
+// and removing the lowest lane that holds it.
+__device__ __forceinline__ float wave_kth_largest(float x, int c) {
+    float r = -INFINITY;
+    for (int q = 0; q < c; ++q) {
+        r = wave_max_f(x);
+        const unsigned long long hold = __builtin_amdgcn_ballot_w64(x == r);
+        const int first = __builtin_amdgcn_readfirstlane(hold ? (int)__builtin_ctzll(hold) : -1);
+        x = (int)__lane_id() == first ? -INFINITY : x;
+    }
+    return r;
 }
 
 // LDS of a slice workgroup and of a merger; a workgroup is one or the
 // other, so the kernel holds them in one union.
-constexpr int kWaves = kThreads / kWave;
 struct SliceLds {
     alignas(16) unsigned long long cand[kCap];      // kWaves regions of kCap / kWaves
     alignas(16) unsigned long long comp[kCap + 2];  // the regions packed
@@ -221,7 +232,8 @@ struct SliceLds {
     uint32_t ban_bits[kSliceMax / 32];
     int nban[kWaves];                               // banned positions held by each wave
     int wcnt[kWaves];
-    float wm[kWaves], ws[kWaves], wt[kWaves];
+    float wm[kWaves], ws[kWaves];
+    float blk[kWave];                               // the 64 block maxima
 };
 struct MergeLds {
     alignas(16) unsigned long long keys[kMergeCap + 2];
@@ -258,7 +270,7 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     uint32_t *ban_bits = L.ban_bits;
     int *nban = L.nban, *wcnt = L.wcnt;
     unsigned long long *cand = L.cand, *comp = L.comp, *best = L.best;
-    float *wm = L.wm, *ws = L.ws, *wt = L.wt;
+    float *wm = L.wm, *ws = L.ws, *blk = L.blk;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int v0 = s * SL, v1 = min(V, v0 + SL), len = max(0, v1 - v0);
@@ -361,20 +373,15 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     }
     const float sw = wave_sum_f(sum);
 
-    // Threshold tau: every value of the slice's c best candidates is at
-    // least tau.  Per wave, the minimum over G lane blocks of the block
-    // maxima has G distinct positions at or above it; with G >= c + (banned
-    // positions in the wave's lanes), c of them are not banned.  A wave with
-    // many bans applies them to its values first (then G >= c).  tau is the
-    // largest of the waves' bounds.
+    // Banned positions cannot be candidates: with any ban in the slice, every
+    // wave turns its banned values into -inf (after the sums, which take
+    // every token) and retakes its lane maxima.
     int nb = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) nb += nban[w];
     nb = __builtin_amdgcn_readfirstlane(nb);
-    const int nbw = __builtin_amdgcn_readfirstlane(nban[wv]);
-    const bool mask_bans = nbw > 0 && c + nbw > 16;
     float cm = m;
-    if (mask_bans) {
+    if (nb > 0) {
         cm = -INFINITY;
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
@@ -387,22 +394,24 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
             }
         }
     }
-    const int need = mask_bans ? c : c + nbw;
-    const float tw = need > kWave ? -INFINITY : block_max_min(cm, need <= 1 ? 0 : 32 - __builtin_clz(need - 1));
+    // Threshold tau: the c-th largest of the slice's 64 block maxima (blocks
+    // of kWaves adjacent lanes of one wave, so kBlocks per wave).  The c
+    // largest blocks each hold a distinct unbanned position at or above tau,
+    // so the slice's c best candidates all lie at or above it.  Every wave
+    // takes the same tau from the same 64 values.
+    const float bm = block_max(cm);
+    if ((lane & (kWaves - 1)) == 0) blk[wv * kBlocks + lane / kWaves] = bm;
     if (lane == 0) {
         wm[wv] = mw;
         ws[wv] = sw;
-        wt[wv] = tw;
     }
     lds_barrier();
-    float tau = wt[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) tau = fmaxf(tau, wt[w]);
+    const float tau = wave_kth_largest(blk[lane], c);
 
     // Collect the positions at or above tau into this wave's region.
     // Positions outside the slice hold -inf, below a finite tau; for tau =
     // -inf they become NaN first, which compares false.  A banned position
-    // is a -inf candidate.
+    // holds -inf, so it is a -inf candidate.
     if (tau == -INFINITY) {
 #pragma unroll
         for (int g = 0; g < kGroups; ++g)
@@ -412,7 +421,6 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
                     val[4 * g + e] = (unsigned)(lbase + offs(4 * g + e) - a) < (unsigned)len ? val[4 * g + e] : NAN;
     }
     unsigned long long *mine = cand + wv * kRegion;
-    const bool check_bans = nb > 0 && !mask_bans;
     int cnt = 0;
     // first one test per load (its four values), gathered as bits of a
     // wave-uniform mask without branches; then only the loads whose bit is
@@ -427,11 +435,6 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         if ((hot >> g) & 1u) {
-            uint32_t bits = 0u;
-            if (check_bans) {
-                const int w0 = lbase + g * kSpan;
-                bits = ban_bits[w0 >> 5] >> (w0 & 31);
-            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int j = 4 * g + e;
@@ -439,9 +442,9 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
                 const unsigned long long hit = __builtin_amdgcn_ballot_w64(ok);
                 const int p = cnt + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(hit >> 32),
                                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)hit, 0u));
-                // (value bits, slice position | banned << 31); the key is
-                // formed when the regions are packed
-                const uint32_t pos = (uint32_t)(lbase + offs(j) - a) | (((bits >> e) & 1u) << 31);
+                // (value bits, slice position); the key is formed when the
+                // regions are packed
+                const uint32_t pos = (uint32_t)(lbase + offs(j) - a);
                 if (ok && p < kRegion) mine[p] = ((unsigned long long)__float_as_uint(val[j]) << 32) | pos;
                 cnt += __popcll(hit);
             }
@@ -462,9 +465,7 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
         // the regions, packed; then each key ranked among all of them
         for (int q = lane; q < cnt; q += kWave) {
             const unsigned long long raw = mine[q];
-            const uint32_t pos = (uint32_t)raw;
-            const float x = (pos >> 31) ? -INFINITY : __uint_as_float((uint32_t)(raw >> 32));
-            comp[before + q] = make_key(x, (uint32_t)v0 + (pos & 0x7fffffffu));
+            comp[before + q] = make_key(__uint_as_float((uint32_t)(raw >> 32)), (uint32_t)v0 + (uint32_t)raw);
         }
         if (tid == 0) comp[total] = 0ull;
         lds_barrier();
@@ -477,13 +478,11 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
         // each round, so no 64-bit key array stays live across the rounds.
 #pragma unroll
         for (int g = 0; g < kGroups; ++g) {
-            const uint32_t bits =
-                check_bans ? ban_bits[(lbase + g * kSpan) >> 5] >> ((lbase + g * kSpan) & 31) : 0u;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int j = 4 * g + e;
                 const bool in = (unsigned)(lbase + offs(j) - a) < (unsigned)len;
-                val[j] = __uint_as_float(in ? ordered(((bits >> e) & 1u) ? -INFINITY : val[j]) : 0u);
+                val[j] = __uint_as_float(in ? ordered(val[j]) : 0u);
             }
         }
         uint32_t last_hi = ~0u, last_lo = ~0u;
@@ -569,15 +568,25 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
         const int e = tid + q * kThreads;
         wv[q] = e < nw ? __hip_atomic_load(recs + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : tag;
     }
+    // re-read every word still without the tag together, so the wait ends
+    // one round trip after the last record lands
+    constexpr unsigned long long kHi = 0xffffffff00000000ull;
+    for (int spin = 0; spin < kMaxSpins; ++spin) {
+        bool pending = false;
+#pragma unroll
+        for (int q = 0; q < kPerThread; ++q) pending |= (wv[q] & kHi) != tag;
+        if (!pending) break;
+        __builtin_amdgcn_s_sleep(2);
+#pragma unroll
+        for (int q = 0; q < kPerThread; ++q)
+            if ((wv[q] & kHi) != tag)
+                wv[q] = __hip_atomic_load(recs + tid + q * kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     bool old = false;
 #pragma unroll
     for (int q = 0; q < kPerThread; ++q) {
         const int e = tid + q * kThreads;
-        for (int spin = 0; (wv[q] & 0xffffffff00000000ull) != tag && spin < kMaxSpins; ++spin) {
-            __builtin_amdgcn_s_sleep(2);
-            wv[q] = __hip_atomic_load(recs + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        old |= (wv[q] & 0xffffffff00000000ull) != tag;
+        old |= (wv[q] & kHi) != tag;
         if (e < nw) w32[e] = (uint32_t)wv[q];
     }
     __syncthreads();
