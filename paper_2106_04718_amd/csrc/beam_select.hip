@@ -48,12 +48,12 @@ namespace fs {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kThreads = 256;
-constexpr int kPer = 64;                 // logits per thread and slice
+constexpr int kThreads = 512;
+constexpr int kPer = 32;                 // logits per thread and slice
 constexpr int kSliceMax = kThreads * kPer;
 constexpr int kCap = 1024;               // collected candidates per slice before the exact path
 constexpr int kMergeCap = 1024;          // candidates a merger ranks: k * slices * c
-constexpr int kMergeWords = 8 * kThreads; // record words a merger reads: k * slices * (2 + 2c)
+constexpr int kMergeWords = 2048;        // record words a merger reads: k * slices * (2 + 2c)
 constexpr int kMaxSpins = 1 << 14;       // bounded re-reads of a record word (about 10 ms)
 constexpr int kNMax = 8;                 // n-gram sizes whose first window is loaded ahead
 constexpr int kWaves = kThreads / kWave;
@@ -140,6 +140,17 @@ __device__ __forceinline__ float wave_sum_f(float x) {
     }
 }
 
+template <int STEP = 0>
+__device__ __forceinline__ uint32_t wave_or(uint32_t x) {
+    if constexpr (STEP == 6) {
+        return x;
+    } else {
+        uint32_t p, unused;
+        partner<STEP>(p, unused, x, 0u);
+        return wave_or<STEP + 1>(x | p);
+    }
+}
+
 __device__ __forceinline__ void store_word(unsigned long long *p, unsigned long long tag, uint32_t v) {
     __hip_atomic_store(p, tag | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -209,31 +220,17 @@ __device__ __forceinline__ float block_max(float x) {
     }
 }
 
-// The c-th largest of the wave's 64 lane values, counted with multiplicity
-// (1 <= c <= 64; no value is NaN): c rounds, each taking the wave maximum
-// and removing the lowest lane that holds it.
-__device__ __forceinline__ float wave_kth_largest(float x, int c) {
-    float r = -INFINITY;
-    for (int q = 0; q < c; ++q) {
-        r = wave_max_f(x);
-        const unsigned long long hold = __builtin_amdgcn_ballot_w64(x == r);
-        const int first = __builtin_amdgcn_readfirstlane(hold ? (int)__builtin_ctzll(hold) : -1);
-        x = (int)__lane_id() == first ? -INFINITY : x;
-    }
-    return r;
-}
-
 // LDS of a slice workgroup and of a merger; a workgroup is one or the
 // other, so the kernel holds them in one union.
 struct SliceLds {
-    alignas(16) unsigned long long cand[kCap];      // kWaves regions of kCap / kWaves
-    alignas(16) unsigned long long comp[kCap + 2];  // the regions packed
+    alignas(16) unsigned long long comp[kCap + 2 + kWave];  // candidate keys, then one spare slot per lane
+    alignas(16) unsigned long long bkey[kWave];     // the 64 block maxima as keys
     unsigned long long best[16];
+    unsigned long long xwin[kWaves];                // exact path: each wave's best key of a round
     uint32_t ban_bits[kSliceMax / 32];
     int nban[kWaves];                               // banned positions held by each wave
-    int wcnt[kWaves];
+    int ncand;
     float wm[kWaves], ws[kWaves];
-    float blk[kWave];                               // the 64 block maxima
 };
 struct MergeLds {
     alignas(16) unsigned long long keys[kMergeCap + 2];
@@ -265,12 +262,11 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
 {
     constexpr int kGroups = kPer / 4;          // 16-byte loads per thread
     constexpr int kSpan = kThreads * 4;        // window positions per load
-    constexpr int kRegion = kCap / kWaves;     // collected candidates per wave
     constexpr float kLog2e = 1.4426950408889634f;
     uint32_t *ban_bits = L.ban_bits;
-    int *nban = L.nban, *wcnt = L.wcnt;
-    unsigned long long *cand = L.cand, *comp = L.comp, *best = L.best;
-    float *wm = L.wm, *ws = L.ws, *blk = L.blk;
+    int *nban = L.nban;
+    unsigned long long *comp = L.comp, *best = L.best, *bkey = L.bkey, *xwin = L.xwin;
+    float *wm = L.wm, *ws = L.ws;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int v0 = s * SL, v1 = min(V, v0 + SL), len = max(0, v1 - v0);
@@ -312,6 +308,7 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     for (int i = tid; i < (wl + 31) / 32; i += kThreads) ban_bits[i] = 0u;
     if (tid < 16) best[tid] = 0ull;
     if (tid < kWaves) nban[tid] = 0;
+    if (tid == 0) L.ncand = 0;
     lds_barrier();
     if (bans) {
         const int suffix = t - n + 1;
@@ -375,7 +372,7 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
 
     // Banned positions cannot be candidates: with any ban in the slice, every
     // wave turns its banned values into -inf (after the sums, which take
-    // every token) and retakes its lane maxima.
+    // every token) and retakes its load maxima.
     int nb = 0;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) nb += nban[w];
@@ -397,21 +394,38 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     // Threshold tau: the c-th largest of the slice's 64 block maxima (blocks
     // of kWaves adjacent lanes of one wave, so kBlocks per wave).  The c
     // largest blocks each hold a distinct unbanned position at or above tau,
-    // so the slice's c best candidates all lie at or above it.  Every wave
-    // takes the same tau from the same 64 values.
+    // so the slice's c best candidates all lie at or above it.  Each lane
+    // ranks one block maximum (as a key with its block index, so the 64 keys
+    // are distinct) against all 64; every wave finds the same tau.
     const float bm = block_max(cm);
-    if ((lane & (kWaves - 1)) == 0) blk[wv * kBlocks + lane / kWaves] = bm;
+    const int bidx = wv * kBlocks + lane / kWaves;
+    if ((lane & (kWaves - 1)) == 0) bkey[bidx] = ((unsigned long long)ordered(bm) << 32) | (uint32_t)~bidx;
     if (lane == 0) {
         wm[wv] = mw;
         ws[wv] = sw;
     }
     lds_barrier();
-    const float tau = wave_kth_largest(blk[lane], c);
+    float tau;
+    {
+        const unsigned long long mine = bkey[lane];
+        const ulonglong2 *b2 = reinterpret_cast<const ulonglong2 *>(bkey);
+        int rank = 0;
+#pragma unroll
+        for (int q = 0; q < kWave / 2; ++q) {
+            const ulonglong2 o = b2[q];
+            rank += (o.x > mine) + (o.y > mine);
+        }
+        const unsigned long long at = __builtin_amdgcn_ballot_w64(rank == c - 1);
+        const int src = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(at));   // one lane: the keys are distinct
+        tau = unordered((uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(mine >> 32), src));
+    }
 
-    // Collect the positions at or above tau into this wave's region.
-    // Positions outside the slice hold -inf, below a finite tau; for tau =
-    // -inf they become NaN first, which compares false.  A banned position
-    // holds -inf, so it is a -inf candidate.
+    // Collect the positions at or above tau as keys.  Positions outside the
+    // slice hold -inf, below a finite tau; for tau = -inf they become NaN
+    // first, which compares false.  A banned position holds -inf, so it is a
+    // -inf candidate.  Each lane takes its places with one LDS atomic; a
+    // value below tau is written to the lane's spare slot instead, so the
+    // stores need no branch.
     if (tau == -INFINITY) {
 #pragma unroll
         for (int g = 0; g < kGroups; ++g)
@@ -420,104 +434,119 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
                 for (int e = 0; e < 4; ++e)
                     val[4 * g + e] = (unsigned)(lbase + offs(4 * g + e) - a) < (unsigned)len ? val[4 * g + e] : NAN;
     }
-    unsigned long long *mine = cand + wv * kRegion;
-    int cnt = 0;
-    // first one test per load (its four values), gathered as bits of a
-    // wave-uniform mask without branches; then only the loads whose bit is
-    // set, value by value
-    uint32_t hot = 0u;
+    uint32_t lhot = 0u;   // this lane's loads holding a value at or above tau
+#pragma unroll
+    for (int g = 0; g < kGroups; ++g) lhot |= (g < ng && gm[g] >= tau) ? 1u << g : 0u;
+    const uint32_t hot = __builtin_amdgcn_readfirstlane(wave_or(lhot));
+    int nh = 0;
 #pragma unroll
     for (int g = 0; g < kGroups; ++g)
-        hot |= (g < ng && __builtin_amdgcn_ballot_w64(gm[g] >= tau) != 0) ? 1u << g : 0u;
-    hot = __builtin_amdgcn_readfirstlane(hot);
-    // a hot load: each of its four values at or above tau is written at the
-    // wave's next free places, by predicated stores (no branch per value)
+        if ((hot >> g) & 1u)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) nh += val[4 * g + e] >= tau;
+    int at = 0;
+    if (nh > 0) at = atomicAdd(&L.ncand, nh);
 #pragma unroll
     for (int g = 0; g < kGroups; ++g) {
         if ((hot >> g) & 1u) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int j = 4 * g + e;
-                const bool ok = val[j] >= tau;
-                const unsigned long long hit = __builtin_amdgcn_ballot_w64(ok);
-                const int p = cnt + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(hit >> 32),
-                                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)hit, 0u));
-                // (value bits, slice position); the key is formed when the
-                // regions are packed
-                const uint32_t pos = (uint32_t)(lbase + offs(j) - a);
-                if (ok && p < kRegion) mine[p] = ((unsigned long long)__float_as_uint(val[j]) << 32) | pos;
-                cnt += __popcll(hit);
+                const bool ok = val[j] >= tau && at < kCap;
+                comp[ok ? at : kCap + 2 + lane] = make_key(val[j], (uint32_t)(v0 + lbase + offs(j) - a));
+                at += ok;
             }
-        }
-    }
-    if (lane == 0) wcnt[wv] = cnt;
-    lds_barrier();
-    int total = 0, before = 0;
-    bool over = false;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-        const int cw = wcnt[w];
-        before += w < wv ? cw : 0;
-        total += cw;
-        over |= cw > kRegion;
-    }
-    if (!over) {
-        // the regions, packed; then each key ranked among all of them
-        for (int q = lane; q < cnt; q += kWave) {
-            const unsigned long long raw = mine[q];
-            comp[before + q] = make_key(__uint_as_float((uint32_t)(raw >> 32)), (uint32_t)v0 + (uint32_t)raw);
-        }
-        if (tid == 0) comp[total] = 0ull;
-        lds_barrier();
-        rank_top_keys(comp, total, c, best);
-    } else {
-        // Exact path (many values at the threshold, e.g. equal logits): c
-        // rounds, each taking the best key below the last one.  The values
-        // become their order-preserving bits in place (0 outside the slice,
-        // below every position's) and the index half of a key is formed in
-        // each round, so no 64-bit key array stays live across the rounds.
-#pragma unroll
-        for (int g = 0; g < kGroups; ++g) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int j = 4 * g + e;
-                const bool in = (unsigned)(lbase + offs(j) - a) < (unsigned)len;
-                val[j] = __uint_as_float(in ? ordered(val[j]) : 0u);
-            }
-        }
-        uint32_t last_hi = ~0u, last_lo = ~0u;
-        for (int q = 0; q < c; ++q) {
-            // ~index of offset 0 (~(i + d) = ~i - d), opaque to the compiler in
-            // each round so that the 64 index halves are not kept across rounds
-            uint32_t lo0 = ~(uint32_t)(v0 + lbase - a);
-            asm volatile("" : "+v"(lo0));
-            // (bh, bl) starts below every key whose high half is not 0, and
-            // positions outside the slice (high half 0) never rise above it
-            uint32_t bh = 0u, bl = ~0u;
-#pragma unroll
-            for (int j = 0; j < kPer; ++j) {
-                const uint32_t hi = __float_as_uint(val[j]);
-                const uint32_t lo = lo0 - (uint32_t)offs(j);
-                const bool below = hi < last_hi || (hi == last_hi && lo < last_lo);
-                const bool above = hi > bh || (hi == bh && lo > bl);
-                bh = below && above ? hi : bh;
-                bl = below && above ? lo : bl;
-            }
-            const unsigned long long b = wave_max_key(bh ? ((unsigned long long)bh << 32) | bl : 0ull);
-            __syncthreads();  // the previous round's reads of cand are done
-            if (lane == 0) cand[wv] = b;
-            __syncthreads();
-            unsigned long long wmax = cand[0];
-#pragma unroll
-            for (int w = 1; w < kWaves; ++w) wmax = cand[w] > wmax ? cand[w] : wmax;
-            if (tid == 0) best[q] = wmax;
-            last_hi = (uint32_t)(wmax >> 32);
-            last_lo = (uint32_t)wmax;
         }
     }
     lds_barrier();
-    // the record of (r, s)
+    const int total = L.ncand;
     unsigned long long *rec = part + ((size_t)r * NS + s) * rec_words(c);
+    if (total <= kWave) {
+        // Few candidates: wave 0 ranks them in registers and writes the
+        // record; the other waves are done.
+        if (wv != 0) return;
+        const unsigned long long ke = lane < total ? comp[lane] : 0ull;
+        const ulonglong2 *k2 = reinterpret_cast<const ulonglong2 *>(comp);
+        int rank = 0;
+        for (int q = 0; q < (total + 1) / 2; ++q) {
+            const ulonglong2 o = k2[q];
+            rank += (o.x > ke) + (q * 2 + 1 < total && o.y > ke);
+        }
+        if (lane < total && rank < c) {
+            store_word(rec + 2 + rank, tag, __float_as_uint(unordered((uint32_t)(ke >> 32))));
+            store_word(rec + 2 + c + rank, tag, ~(uint32_t)ke);
+        }
+        // an empty slot (fewer positions than c) is a -inf value at index ~0
+        if (lane >= total && lane < c) {
+            store_word(rec + 2 + lane, tag, __float_as_uint(-INFINITY));
+            store_word(rec + 2 + c + lane, tag, 0xffffffffu);
+        }
+    } else {
+        if (total <= kCap) {
+            // the keys ranked among themselves by every thread
+            if (tid == 0) {
+                comp[total] = 0ull;
+                comp[total + 1] = 0ull;
+            }
+            if (tid < 16) best[tid] = 0ull;
+            lds_barrier();
+            rank_top_keys(comp, total, c, best);
+        } else {
+            // Exact path (more than kCap values at the threshold, e.g. equal
+            // logits): c rounds, each taking the best key below the last one.
+            // The values become their order-preserving bits in place (0
+            // outside the slice, below every position's) and the index half of
+            // a key is formed in each round, so no 64-bit key array stays live
+            // across the rounds.
+#pragma unroll
+            for (int g = 0; g < kGroups; ++g) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int j = 4 * g + e;
+                    const bool in = (unsigned)(lbase + offs(j) - a) < (unsigned)len;
+                    val[j] = __uint_as_float(in ? ordered(val[j]) : 0u);
+                }
+            }
+            uint32_t last_hi = ~0u, last_lo = ~0u;
+            for (int q = 0; q < c; ++q) {
+                // ~index of offset 0 (~(i + d) = ~i - d), opaque to the compiler in
+                // each round so that the 64 index halves are not kept across rounds
+                uint32_t lo0 = ~(uint32_t)(v0 + lbase - a);
+                asm volatile("" : "+v"(lo0));
+                // (bh, bl) starts below every key whose high half is not 0, and
+                // positions outside the slice (high half 0) never rise above it
+                uint32_t bh = 0u, bl = ~0u;
+#pragma unroll
+                for (int j = 0; j < kPer; ++j) {
+                    const uint32_t hi = __float_as_uint(val[j]);
+                    const uint32_t lo = lo0 - (uint32_t)offs(j);
+                    const bool below = hi < last_hi || (hi == last_hi && lo < last_lo);
+                    const bool above = hi > bh || (hi == bh && lo > bl);
+                    bh = below && above ? hi : bh;
+                    bl = below && above ? lo : bl;
+                }
+                const unsigned long long b = wave_max_key(bh ? ((unsigned long long)bh << 32) | bl : 0ull);
+                __syncthreads();  // the previous round's reads of xwin are done
+                if (lane == 0) xwin[wv] = b;
+                __syncthreads();
+                unsigned long long wmax = xwin[0];
+#pragma unroll
+                for (int w = 1; w < kWaves; ++w) wmax = xwin[w] > wmax ? xwin[w] : wmax;
+                if (tid == 0) best[q] = wmax;
+                last_hi = (uint32_t)(wmax >> 32);
+                last_lo = (uint32_t)wmax;
+            }
+        }
+        lds_barrier();
+        if (tid < c) {
+            const unsigned long long kk = best[tid];
+            // an empty key (fewer positions than c) is a -inf value at index ~0
+            store_word(rec + 2 + tid, tag, kk ? __float_as_uint(unordered((uint32_t)(kk >> 32)))
+                                              : __float_as_uint(-INFINITY));
+            store_word(rec + 2 + c + tid, tag, kk ? ~(uint32_t)kk : 0xffffffffu);
+        }
+    }
+    // the slice's (max, sum of exp): the waves' sums rescaled to the slice maximum
     if (tid == 0) {
         float M = wm[0];
 #pragma unroll
@@ -528,13 +557,6 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
             S += wm[w] == -INFINITY ? 0.f : ws[w] * __builtin_amdgcn_exp2f((wm[w] - M) * kLog2e);
         store_word(rec, tag, __float_as_uint(M));
         store_word(rec + 1, tag, __float_as_uint(S));
-    }
-    if (tid < c) {
-        const unsigned long long kk = best[tid];
-        const uint32_t o = (uint32_t)(kk >> 32);
-        // an empty key (fewer positions than c) is a -inf value at index 0
-        store_word(rec + 2 + tid, tag, kk ? __float_as_uint(unordered(o)) : __float_as_uint(-INFINITY));
-        store_word(rec + 2 + c + tid, tag, kk ? ~(uint32_t)kk : 0xffffffffu);
     }
 }
 
