@@ -2,7 +2,12 @@
 
 Plain ``-O2`` without fast-math, so libm's ``exp`` and IEEE fp64 arithmetic are
 used as written.  OpenMP spreads independent rows over host threads.
+
+``build(sanitize=True)`` (``python oracle/build.py --sanitize``) compiles it
+with clang, AddressSanitizer and UndefinedBehaviorSanitizer instead (the same
+runtime as the sanitized HIP library, so both load into one process).
 """
+import os
 import pathlib
 import subprocess
 
@@ -11,8 +16,14 @@ SRC = HERE / "oracle.c"
 LIB = HERE / "liboracle.so"
 
 
-def build(verbose: bool = False) -> pathlib.Path:
-    cmd = ["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared",
+def build(verbose: bool = False, sanitize: bool = False) -> pathlib.Path:
+    if sanitize:
+        clang = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "bin", "clang")
+        cc = [clang, "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-shared-libasan",
+              "-fno-omit-frame-pointer"]
+    else:
+        cc = ["gcc"]
+    cmd = [*cc, "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared",
            "-Wall", "-Wextra", "-Werror", str(SRC), "-o", str(LIB) + ".tmp", "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -22,4 +33,5 @@ def build(verbose: bool = False) -> pathlib.Path:
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv[1:]))

@@ -6,6 +6,14 @@ pass warns that it does not know that feature, which is harmless.
 
 The CPython marshalling module (csrc/pyext.c, plain C) is then compiled with
 gcc and linked against the library.
+
+``build(sanitize=True)`` (``python -m paper_2106_04718_amd.build --sanitize``)
+instruments the host code of every source with AddressSanitizer and
+UndefinedBehaviorSanitizer (``-Xarch_host``: device code is built as usual),
+links the library against clang's shared sanitizer runtime and builds the
+marshalling module with clang and the same sanitizers.  Such a build is for
+CPU test runs only (tests/run_sanitized.sh); a plain ``build()`` restores the
+normal library.
 """
 import concurrent.futures
 import os
@@ -37,9 +45,29 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def _compile(src: str, verbose: bool) -> pathlib.Path:
+# host-side sanitizer flags: every one behind -Xarch_host, so no device code
+# is built with a sanitizer
+SANITIZE_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
+SANITIZE_LINK = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-shared-libasan"]
+
+
+def clang() -> str:
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    return os.path.join(rocm, "llvm", "bin", "clang")
+
+
+def sanitizer_runtime() -> str:
+    """Path of clang's shared AddressSanitizer runtime (to preload into python)."""
+    return subprocess.run([clang(), "-print-file-name=libclang_rt.asan-x86_64.so"], check=True,
+                          capture_output=True, text=True).stdout.strip()
+
+
+def _compile(src: str, verbose: bool, sanitize: bool = False) -> pathlib.Path:
     obj = BUILD / (src + ".o")
-    cmd = [hipcc(), *COMMON, "-x", "hip", "-c", str(CSRC / src), "-o", str(obj)]
+    cmd = [hipcc(), *COMMON, *(SANITIZE_HOST if sanitize else []), "-x", "hip", "-c", str(CSRC / src),
+           "-o", str(obj)]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -52,25 +80,27 @@ def _compile(src: str, verbose: bool) -> pathlib.Path:
     return obj
 
 
-def build(verbose: bool = False) -> pathlib.Path:
+def build(verbose: bool = False, sanitize: bool = False) -> pathlib.Path:
     BUILD.mkdir(exist_ok=True)
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+        objs = list(ex.map(lambda s: _compile(s, verbose, sanitize), SOURCES))
     tmp = str(LIB) + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-Wl,-soname,libfastseq_hip.so",
-           *map(str, objs), "-o", tmp]
+           *(SANITIZE_LINK if sanitize else []), *map(str, objs), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
-    build_ext(verbose)
+    build_ext(verbose, sanitize)
     return LIB
 
 
-def build_ext(verbose: bool = False) -> pathlib.Path:
+def build_ext(verbose: bool = False, sanitize: bool = False) -> pathlib.Path:
     """The CPython module that marshals arguments into the C ABI."""
     tmp = str(EXT) + ".tmp"
-    cmd = ["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror",
+    cc = [clang(), "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-shared-libasan",
+          "-fno-omit-frame-pointer"] if sanitize else ["gcc"]
+    cmd = [*cc, "-std=c11", "-O2", "-fPIC", "-shared", "-Wall", "-Wextra", "-Werror",
            f"-I{sysconfig.get_paths()['include']}", f"-I{ROOT / 'include'}", str(CSRC / "pyext.c"),
            f"-L{PKG}", "-lfastseq_hip", "-Wl,-rpath,$ORIGIN", "-o", tmp]
     if verbose:
@@ -81,4 +111,5 @@ def build_ext(verbose: bool = False) -> pathlib.Path:
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    import sys
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv[1:]))
