@@ -43,14 +43,17 @@
  *     in fs_last_error().
  *   - Calls are re-entrant; calls on different streams may run concurrently
  *     as long as they do not share an output or workspace buffer.
- *   - Graph capture: fs_ngram_block, fs_cache_reorder, fs_beam_ancestry_step
- *     and the attention calls that take one workgroup per row (128 or more
- *     (source, head) rows) keep no state between calls and may be captured
- *     into a HIP graph and replayed.  Calls whose workgroups exchange tagged
- *     records through the workspace (the attention's split-KV form for
- *     fewer rows, and fs_beam_select) tell their own records apart by a tag
- *     passed at launch, which a graph would freeze; they return
- *     FS_ERR_UNSUPPORTED when `stream` is capturing, before any launch.
+ *   - Graph capture: every call may be captured into a HIP graph and
+ *     replayed (FS_VALIDATE mode aside).  Calls whose workgroups exchange
+ *     tagged records through the workspace (the attention's split-KV form
+ *     for fewer than 128 (source, head) rows, and fs_beam_select) tag them,
+ *     when captured, by a counter per row or source kept at the end of the
+ *     workspace, which each replay advances on the device; eager calls tag
+ *     them by a host epoch, and the two kinds of tag never coincide.  A
+ *     workspace used by captured calls must keep serving calls of the same
+ *     sizes while the graph is replayed (zero-fill it again before it serves
+ *     other sizes under capture), and a graph's replays must not overlap
+ *     other calls on the same workspace.
  *   - Debug mode: with the environment variable FS_VALIDATE=1 set when the
  *     library is first used (or after fs_set_tuning(FS_TUNE_VALIDATE, 1)),
  *     the attention calls copy src_len / prefix_len
@@ -74,7 +77,7 @@ typedef enum {
     FS_OK = 0,
     FS_ERR_INVALID_ARG = 1,  /* bad pointer, size, alignment, aliasing or workspace */
     FS_ERR_UNSUPPORTED = 2,  /* valid but not implemented: D, k or dtype outside the set below,
-                                or a record-exchanging call under stream capture */
+                                or FS_VALIDATE mode under stream capture */
     FS_ERR_HIP = 3           /* a HIP runtime call or kernel launch failed */
 } fs_status_t;
 
@@ -122,12 +125,14 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  *   out      [B, k, H, D]  dtype    result, rounded to nearest-even from fp32
  *   workspace, workspace_bytes      scratch of at least
  *            fs_beam_cross_attn_workspace_bytes(B, k, H, S, D, dtype)
- *            bytes (per-tile partials).  It must be zero-filled once
+ *            bytes (per-tile partials, then a counter per (source, head)
+ *            row for captured calls).  It must be zero-filled once
  *            before its first use and not written by anything else after
  *            that: each call marks the words it writes with a tag of its
  *            own, and an all-zero or earlier-tagged word is never taken as
- *            this call's (a tag repeats only after 2^32 calls in one
- *            process).  Any size-compatible call may reuse it (also of
+ *            this call's (an eager call's tag repeats only after 2^31 calls
+ *            in one process, a captured call's after 2^31 replays).  Any
+ *            size-compatible call may reuse it (also of
  *            fs_beam_prefix_attn).  Calls that share a workspace must not
  *            run concurrently.
  *   stream   hipStream_t (NULL = default stream)
@@ -142,8 +147,7 @@ size_t fs_beam_cross_attn_workspace_bytes(int B, int k, int H, int S, int D, int
  * negative sizes, a pointer of q/K/V/out/workspace not 16-byte aligned, a
  * workspace that is too small, or out or the workspace overlapping another
  * argument; sizes too large for one launch;
- * FS_ERR_UNSUPPORTED for D, k or dtype outside the set above, or for the
- * split-KV form (fewer than 128 rows) while `stream` is capturing; FS_ERR_HIP
+ * FS_ERR_UNSUPPORTED for D, k or dtype outside the set above; FS_ERR_HIP
  * for a failed launch.  B == 0, k == 0 or H == 0 returns FS_OK with no launch.
  */
 int fs_beam_cross_attn(const void *q, const void *K, const void *V,
@@ -296,7 +300,8 @@ int fs_set_tuning(int knob, int value);
 
 /*
  * Workspace, in bytes, that fs_beam_select needs for these sizes (per
- * (hypothesis, vocabulary slice) partial records).  Zero-fill it before its
+ * (hypothesis, vocabulary slice) partial records, then a counter per source
+ * for captured calls).  Zero-fill it before its
  * first use; the reuse rules are those of fs_beam_cross_attn's workspace.
  * 0 for empty problems; (size_t)-1 for invalid or unsupported sizes.
  */
@@ -342,8 +347,7 @@ size_t fs_beam_select_workspace_bytes(int B, int k, int V, int c);
  * sizes, n < 0, ld_tokens < t with n > 0, c > k*V, pointers not 4-byte
  * aligned, a workspace that is too small, or an output overlapping an input
  * or another output; FS_ERR_UNSUPPORTED for c, k or the candidate count
- * outside the set above, or while `stream` is capturing; FS_ERR_HIP for a
- * failed launch.  B == 0 returns
+ * outside the set above; FS_ERR_HIP for a failed launch.  B == 0 returns
  * FS_OK with no launch.  If a partial record is not seen within about 10 ms
  * (which does not happen in a working launch), the source's outputs are NaN
  * and -1.

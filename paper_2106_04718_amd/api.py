@@ -51,7 +51,9 @@ def new_workspace(nbytes: int, device) -> torch.Tensor:
 
     The library tags every word it writes with its call, so a workspace
     needs zero-filling only once, before its first use; reuse it across
-    calls (of any size that fits) without clearing.
+    calls (of any size that fits) without clearing.  A workspace of calls
+    captured into a graph must keep serving calls of the same sizes while
+    the graph is replayed.
     """
     return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 

@@ -151,6 +151,17 @@ __device__ __forceinline__ uint32_t wave_or(uint32_t x) {
     }
 }
 
+// Tag of the record words of a call, in their high 32 bits: the host's epoch
+// in [1, 2^31), or, for a call captured into a graph (epoch 0), the source's
+// counter in the workspace with bit 31 set, which the source's merger
+// advances once it has every record.  c0 receives the counter value.
+__device__ __forceinline__ unsigned long long call_tag(unsigned long long epoch, const unsigned long long *ctr,
+                                                       unsigned long long &c0) {
+    if (epoch != 0) return (epoch & 0xffffffffull) << 32;
+    c0 = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (0x80000000ull | ((c0 % 0x7fffffffull) + 1)) << 32;
+}
+
 __device__ __forceinline__ void store_word(unsigned long long *p, unsigned long long tag, uint32_t v) {
     __hip_atomic_store(p, tag | v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -709,16 +720,23 @@ __global__ __launch_bounds__(kThreads) void beam_select_kernel(
     const float *__restrict__ logits, const float *__restrict__ beam_scores, const int32_t *__restrict__ tokens,
     int ld, int t, int n, float *__restrict__ out_scores, int32_t *__restrict__ out_beam,
     int32_t *__restrict__ out_token, unsigned long long *__restrict__ part, int rows, int k, int V, int c,
-    int NS, int SL, unsigned long long epoch)
+    int NS, int SL, unsigned long long epoch, unsigned long long *__restrict__ ctr)
 {
     __shared__ SelectLds lds;
-    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     const int g = blockIdx.x;
+    const int b = g < rows * NS ? g / NS / k : g - rows * NS;
+    unsigned long long c0 = 0;
+    const unsigned long long tag = call_tag(epoch, ctr + b, c0);
     if (g < rows * NS) {
         select_slice(lds.slice, logits, tokens, ld, t, n, part, g / NS, g % NS, V, c, NS, SL, tag);
     } else {
-        select_merge(lds.merge, beam_scores, part, out_scores, out_beam, out_token, g - rows * NS, k, V, c, NS,
-                     tag);
+        select_merge(lds.merge, beam_scores, part, out_scores, out_beam, out_token, b, k, V, c, NS, tag);
+        // a captured call: the merger has every record (or its wait ran
+        // out), so every slice of the source has read the counter; the next
+        // call takes the next value (skipping one after a wait that ran out,
+        // so that a late record of this call never passes for the next's)
+        if (epoch == 0 && threadIdx.x == 0)
+            __hip_atomic_store(ctr + b, c0 + (lds.merge.stale ? 2 : 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -755,7 +773,7 @@ int beam_select_max_record_words() { return kMergeWords; }
 
 size_t beam_select_workspace_words(int B, int k, int V, int c) {
     const int NS = beam_select_slices(B * k, V, k, c);
-    return (size_t)B * k * NS * rec_words(c);
+    return (size_t)B * k * NS * rec_words(c) + B;   // the records, then one counter per source
 }
 
 hipError_t launch_beam_select(const float *logits, const float *beam_scores, const int32_t *tokens, int ld,
@@ -767,8 +785,10 @@ hipError_t launch_beam_select(const float *logits, const float *beam_scores, con
     const int NS = beam_select_slices(rows, V, k, c);
     const int SL = (V + NS - 1) / NS;
     const long long nblk = (long long)rows * NS + B;
+    unsigned long long *ctr = workspace + (size_t)rows * NS * rec_words(c);
     hipLaunchKernelGGL(beam_select_kernel, dim3((unsigned)nblk), dim3(kThreads), 0, stream, logits, beam_scores,
-                       tokens, ld, t, n, out_scores, out_beam, out_token, workspace, rows, k, V, c, NS, SL, epoch);
+                       tokens, ld, t, n, out_scores, out_beam, out_token, workspace, rows, k, V, c, NS, SL, epoch,
+                       ctr);
     return hipGetLastError();
 }
 

@@ -70,15 +70,13 @@ bool validate_mode() {
 }
 
 // Epochs tag the partial records in the workspace: every call gets a fresh
-// nonzero epoch, so a workspace zero-filled once never needs clearing again
-// (a zero word, or one left by an earlier call, never carries this call's tag).
-std::atomic<unsigned long long> g_epoch{1};
+// epoch in [1, 2^31), so a workspace zero-filled once never needs clearing
+// again (a zero word, or one left by an earlier call, never carries this
+// call's tag).  Tags with bit 31 set belong to captured calls (below).
+std::atomic<unsigned long long> g_epoch{0};
 
 unsigned long long next_epoch() {
-    for (;;) {
-        const unsigned long long e = g_epoch.fetch_add(1, std::memory_order_relaxed) & 0xffffffffull;
-        if (e != 0) return e;
-    }
+    return g_epoch.fetch_add(1, std::memory_order_relaxed) % 0x7fffffffull + 1;
 }
 
 bool supported_d(int D) { return D == 16 || D == 32 || D == 64 || D == 128; }
@@ -91,13 +89,19 @@ static_assert((int)fs::AttnPath::kSplit == FS_ATTN_PATH_SPLIT && (int)fs::AttnPa
                   (int)fs::AttnPath::kWhole2 == FS_ATTN_PATH_WHOLE2 && (int)fs::AttnPath::kWhole4 == FS_ATTN_PATH_WHOLE4,
               "the tuning values name the decompositions");
 
-// A call whose kernels exchange tagged records through the workspace tells
-// its own records from older ones by a tag passed at launch.  Under stream
-// capture that tag would be frozen into the graph, and a replay could take
-// the previous replay's records for its own: such calls are refused there.
 bool capturing(hipStream_t s) {
     hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
     return hipStreamIsCapturing(s, &st) == hipSuccess && st != hipStreamCaptureStatusNone;
+}
+
+// A call whose kernels exchange tagged records through the workspace tells
+// its own records from older ones by a tag.  Eager calls get a host epoch.
+// Under stream capture an epoch would be frozen into the graph, and a
+// replay could take the previous replay's records for its own, so a
+// captured call passes 0: its kernels then tag by per-row counters kept in
+// the workspace, which advance on the device at every replay.
+unsigned long long call_epoch(hipStream_t s) {
+    return capturing(s) ? 0ull : next_epoch();
 }
 
 // Decomposition of an attention call of n_bh rows over S keys (plus a
@@ -253,12 +257,9 @@ int fs_beam_cross_attn(const void *q, const void *K, const void *V, const int32_
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int esize = dtype == FS_BF16 ? 2 : 4;
     const fs::AttnPath path = attn_path_for(B * H, S, D, esize, false);
-    if (path == fs::AttnPath::kSplit && capturing(s))
-        return fail(FS_ERR_UNSUPPORTED, "fs_beam_cross_attn: %d rows take the split-KV form, whose tagged records "
-                    "cannot be captured into a graph", B * H);
     if (validate_mode() && (st = validate_lengths(src_len, B, S, s, "src_len")) != FS_OK) return st;
     hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
-                                         static_cast<float *>(workspace), next_epoch(), s, path);
+                                         static_cast<float *>(workspace), call_epoch(s), s, path);
     if (e != hipSuccess) return hip_fail(e, "fs_beam_cross_attn launch");
     return FS_OK;
 }
@@ -376,14 +377,11 @@ int decode_step(const void *q, const void *K, const void *V, const int32_t *src_
         if (e != hipSuccess) return hip_fail(e, "fs_beam_decode_step n-gram launch");
         return FS_OK;
     }
-    if (path == fs::AttnPath::kSplit && capturing(s))
-        return fail(FS_ERR_UNSUPPORTED, "fs_beam_decode_step: %d rows take the split-KV form, whose tagged records "
-                    "cannot be captured into a graph", B * H);
     if (validate_mode() && (st = validate_lengths(src_len, B, S, s, "src_len")) != FS_OK) return st;
     if (noalloc && path == fs::AttnPath::kSplit && (st = scratch_on(s, &workspace)) != FS_OK) return st;
     const fs::NgramRows ng{tokens, ld_tokens, rows, t, n, logits, vocab};
     hipError_t e = fs::launch_cross_attn(q, K, V, src_len, out, B, k, H, S, D, dtype == FS_BF16,
-                                         static_cast<float *>(workspace), next_epoch(), s, path,
+                                         static_cast<float *>(workspace), call_epoch(s), s, path,
                                          ngram ? &ng : nullptr);
     if (e != hipSuccess) return hip_fail(e, noalloc ? "fs_beam_decode_step_noalloc launch" : "fs_beam_decode_step launch");
     return FS_OK;
@@ -492,13 +490,10 @@ int prefix_attn(const void *q, const void *Kp, const void *Vp, const int32_t *pr
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const fs::AttnPath path = attn_path_for(B * H, N, D, dtype == FS_BF16 ? 2 : 4, t > 0);
-    if (path == fs::AttnPath::kSplit && capturing(s))
-        return fail(FS_ERR_UNSUPPORTED, "%d rows take the split-KV form, whose tagged records cannot be captured "
-                    "into a graph", B * H);
     if (validate_mode() && (st = validate_lengths(prefix_len, B, N, s, "prefix_len")) != FS_OK) return st;
     hipError_t e = fs::launch_prefix_attn(q, Kp, Vp, prefix_len, Kt, Vt, T, t, indirect && t > 0 ? anc : nullptr,
                                           ld_anc, out, B, k, H, N, D, dtype == FS_BF16,
-                                          static_cast<float *>(workspace), next_epoch(), s, path);
+                                          static_cast<float *>(workspace), call_epoch(s), s, path);
     if (e != hipSuccess) return hip_fail(e, indirect ? "fs_beam_prefix_attn_indirect launch" : "fs_beam_prefix_attn launch");
     return FS_OK;
 }
@@ -636,12 +631,10 @@ int fs_beam_select(const float *logits, const float *beam_scores, const int32_t 
         overlaps(workspace, need, tokens, tok_bytes) || overlaps(workspace, need, out_scores, o_bytes) ||
         overlaps(workspace, need, out_beam, o_bytes) || overlaps(workspace, need, out_token, o_bytes))
         return fail(FS_ERR_INVALID_ARG, "workspace overlaps an argument");
-    if (capturing(static_cast<hipStream_t>(stream)))
-        return fail(FS_ERR_UNSUPPORTED, "fs_beam_select exchanges tagged records between its workgroups; it "
-                    "cannot be captured into a graph");
     hipError_t e = fs::launch_beam_select(logits, beam_scores, need_tokens ? tokens : nullptr, ld_tokens, t,
                                           need_tokens ? n : 0, out_scores, out_beam, out_token, B, k, V, c,
-                                          static_cast<unsigned long long *>(workspace), next_epoch(),
+                                          static_cast<unsigned long long *>(workspace),
+                                          call_epoch(static_cast<hipStream_t>(stream)),
                                           static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "fs_beam_select launch");
     return FS_OK;

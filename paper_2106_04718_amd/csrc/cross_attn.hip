@@ -28,7 +28,9 @@
 //   the grid (so dispatched after them), reads the chunks' records, merges
 //   them in chunk order, normalises and writes the output.  Each record word
 //   carries a tag of the call, so the merger knows when a record is
-//   complete; no fence, counter or clearing of the workspace is needed.
+//   complete; no fence or clearing of the workspace is needed.  The tag is
+//   the host's call epoch, or, for a call captured into a graph, a per-row
+//   counter in the workspace that the row's merger advances.
 // Rows j >= src_len[b] are never read.  The chunk size depends only on the
 // row size, and each beam's arithmetic is the same whatever k is, so the
 // output bits do not depend on k, B or the beam's position.
@@ -410,6 +412,19 @@ __device__ __forceinline__ void tile_attend(const uint4 (&qr)[KB], const uint4 *
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Tag of the record words of a call, in their high 32 bits.  Outside graph
+// capture the host passes an epoch in [1, 2^31).  A call captured into a
+// graph passes 0 and takes, for each (b, h) row, that row's counter in the
+// workspace with bit 31 set (so no host epoch equals it); the row's merger
+// advances the counter once it has every record, so each replay of the
+// graph tags its records anew.  c0 receives the counter value.
+__device__ __forceinline__ unsigned long long call_tag(unsigned long long epoch, const unsigned long long *ctr,
+                                                       unsigned long long &c0) {
+    if (epoch != 0) return (epoch & 0xffffffffull) << 32;
+    c0 = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (0x80000000ull | ((c0 % 0x7fffffffull) + 1)) << 32;
+}
+
 // Store one record word (call tag << 32 | fp32 bits) with a device-scope atomic.
 __device__ __forceinline__ void store_word(unsigned long long *p, unsigned long long tag, float v) {
     __hip_atomic_store(p, tag | __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -752,7 +767,7 @@ template <int D, bool BF16, int KB, bool SPLIT>
 __device__ __forceinline__ void merge_chunks(const unsigned long long *__restrict__ part,
                                              const int32_t *__restrict__ src_len, void *__restrict__ out,
                                              int bh, int n_bh, int H, int S, int NT, int t,
-                                             unsigned long long epoch)
+                                             unsigned long long epoch, unsigned long long *__restrict__ ctr)
 {
     using G = Geo<D, BF16>;
     if (bh >= n_bh) return;
@@ -763,8 +778,10 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
     const int nc = (L + G::kTile - 1) / G::kTile;             // tile records of the prefix, in key order
     const int nrec = nc + (SPLIT && t > 0 ? 1 : 0);          // records to merge, in order
     constexpr int kRec = KB * (D + 2);
-    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
+    unsigned long long c0 = 0;
+    const unsigned long long tag = call_tag(epoch, ctr + bh, c0);
     const unsigned long long *recs = part + (size_t)bh * (NT + (SPLIT ? 1 : 0)) * kRec;
+    bool stale_any = false;
     const size_t obase = ((size_t)b * KB * H + h) * D;
     constexpr int kBatch = 4;  // records whose words are loaded together
     for (int x = threadIdx.x; x < KB * D; x += kBlock) {
@@ -805,7 +822,15 @@ __device__ __forceinline__ void merge_chunks(const unsigned long long *__restric
         }
         const float o = nrec == 0 ? 0.f : aa / ll;  // no key at all: zero row
         store_out<BF16>(out, obase + (size_t)i * H * D + d, stale ? NAN : o);
+        stale_any |= stale;
     }
+    // a captured call: every record of the row is in (or the wait ran out),
+    // so every workgroup of the row has read the counter; the next call takes
+    // the next value (skipping one after a wait that ran out, so that a late
+    // record of this call can never pass for the next call's)
+    const int any = __syncthreads_or(stale_any);
+    if (epoch == 0 && threadIdx.x == 0)
+        __hip_atomic_store(ctr + bh, c0 + (any ? 2 : 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Softmax state of one hypothesis over its generated rows, in the compact
@@ -895,7 +920,8 @@ template <int D, bool BF16, int KB, bool ANC>
 __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, const uint4 *__restrict__ Kt,
                                                  const uint4 *__restrict__ Vt, unsigned long long *__restrict__ part,
                                                  int bh, int n_bh, int H, int NT, int T, int t,
-                                                 float scale_log2, unsigned long long epoch, void *lds,
+                                                 float scale_log2, unsigned long long epoch,
+                                                 const unsigned long long *__restrict__ ctr, void *lds,
                                                  const int32_t *__restrict__ anc, int ld_anc)
 {
     if (bh >= n_bh || t <= 0) return;
@@ -904,7 +930,8 @@ __device__ __forceinline__ void attend_generated(const uint4 *__restrict__ q, co
     const int lane = threadIdx.x & (kWave - 1);
     const int w = wave_id();
     constexpr int kRec = KB * (D + 2);
-    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
+    unsigned long long c0;
+    const unsigned long long tag = call_tag(epoch, ctr + bh, c0);
     unsigned long long *rec = part + ((size_t)bh * (NT + 1) + NT) * kRec;
     for (int i = w; i < KB; i += kWaves) {
         GenState<D> gs;
@@ -929,6 +956,7 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     const int32_t *__restrict__ src_len, void *__restrict__ out,
     unsigned long long *__restrict__ part,
     int n_bh, int H, int S, int NC, float scale_log2, unsigned long long epoch,
+    unsigned long long *__restrict__ ctr,
     const uint4 *__restrict__ Kt, const uint4 *__restrict__ Vt, int T, int t, const int32_t *__restrict__ anc,
     int ld_anc, NgramJob ngj)
 {
@@ -959,14 +987,15 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     if constexpr (SPLIT) {
         if (g < n_bh8) {
             attend_generated<D, BF16, KB, ANC>(q, Kt, Vt, part, g, n_bh, H, NC * kWaves, T, t, scale_log2, epoch,
-                                          &t_lds[wave_id()][0], anc, ld_anc);
+                                               ctr, &t_lds[wave_id()][0], anc, ld_anc);
             return;
         }
         g -= n_bh8;
     }
     const int n_chunk_blocks = n_bh8 * NC;
     if (g >= n_chunk_blocks) {
-        merge_chunks<D, BF16, KB, SPLIT>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC * kWaves, t, epoch);
+        merge_chunks<D, BF16, KB, SPLIT>(part, src_len, out, g - n_chunk_blocks, n_bh, H, S, NC * kWaves, t, epoch,
+                                         ctr);
         return;
     }
     const int xcd = g % kXcds;
@@ -989,6 +1018,9 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     }
     if (c >= nc) return;  // chunk lies in the padding: never read
     const int j1 = min(j0 + kChunk, L);
+    // the call's tag (for a captured call a load, issued before the row's)
+    unsigned long long c0;
+    const unsigned long long tag = call_tag(epoch, ctr + bh, c0);
 
     const int lane = tid & (kWave - 1);
     const int w = wave_id();
@@ -1022,7 +1054,6 @@ __global__ __launch_bounds__(kBlock) void cross_attn_kernel(
     // acc[KB][D], then m[KB], then l[KB].
     const int NT = NC * kWaves;
     const int ntile = min(kWaves, (j1 - j0 + kTile - 1) / kTile);   // tiles of this chunk that hold keys
-    const unsigned long long tag = (epoch & 0xffffffffull) << 32;
     for (int ww = 0; ww < ntile; ++ww) {
         unsigned long long *rec = part + ((size_t)bh * (NT + (SPLIT ? 1 : 0)) + c * kWaves + ww) * (KB * (D + 2));
         for (int x = tid; x < KB * D; x += kBlock) {
@@ -1224,6 +1255,8 @@ hipError_t launch_split(const AttnArgs &a, int NC)
     const long long n_bh8 = ((long long)n_bh + kXcds - 1) / kXcds * kXcds;
     const double scale_log2 = 1.4426950408889634074 / sqrt((double)D);
     unsigned long long *part = reinterpret_cast<unsigned long long *>(a.ws);
+    // the rows' counters for captured calls follow the records
+    unsigned long long *ctr = part + (size_t)n_bh * (NC * kWaves + (SPLIT ? 1 : 0)) * (KB * (D + 2));
     // [generated-token workgroups] [chunk workgroups] [mergers]
     const long long mergers = (SPLIT || NC > 1) ? n_bh : 0;
     // n-gram workgroups first, rounded to a multiple of 8 so that the XCD
@@ -1235,7 +1268,7 @@ hipError_t launch_split(const AttnArgs &a, int NC)
     hipLaunchKernelGGL((cross_attn_kernel<D, BF16, KB, SPLIT, ANC>), dim3((unsigned)nblk), dim3(kBlock), 0,
                        a.stream, static_cast<const uint4 *>(a.q), static_cast<const uint4 *>(a.K),
                        static_cast<const uint4 *>(a.V), a.src_len, a.out, part, n_bh, a.H, a.S,
-                       NC, (float)scale_log2, a.epoch, static_cast<const uint4 *>(a.Kt),
+                       NC, (float)scale_log2, a.epoch, ctr, static_cast<const uint4 *>(a.Kt),
                        static_cast<const uint4 *>(a.Vt), a.T, a.t, a.anc, a.ld_anc, ng);
     return hipGetLastError();
 }
@@ -1352,7 +1385,7 @@ size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize,
     const size_t NT = (size_t)std::max(1, (S + C - 1) / C) * kWaves + (split ? 1 : 0);
     const size_t n_bh = (size_t)B * H;
     const size_t part = n_bh * NT * (size_t)k * (size_t)(D + 2);
-    return 2 * part;  // 64-bit partial-record words
+    return 2 * (part + n_bh);  // 64-bit words: the partial records, then one counter per row
 }
 
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V, const int32_t *src_len,

@@ -36,8 +36,9 @@ AttnPath choose_attn_path(int n_bh, int jobs_max);
 AttnPath set_attn_path_override(AttnPath p);
 int set_select_slices_override(int slices);
 
-// Workspace size in 4-byte words: the per-chunk partial records (plus one
-// record per (b, h) for the generated-token segment when `split`).
+// Workspace size in 4-byte words: the per-tile partial records (plus one
+// record per (b, h) for the generated-token segment when `split`), then one
+// 64-bit counter per (b, h) for captured calls.
 size_t cross_attn_workspace_floats(int B, int k, int H, int S, int D, int esize, bool split);
 
 // The n-gram part of a fused decode step (the arguments of fs_ngram_block):
@@ -49,9 +50,10 @@ struct NgramRows {
     int V;
 };
 
-// `epoch` must differ from the epoch of every earlier call that used the
-// same workspace: its low 32 bits tag the partial records, which are never
-// cleared.  With `ngram` (rows > 0, t >= n) the launch also applies the
+// `epoch` in [1, 2^31) must differ from the epoch of every earlier call that
+// used the same workspace: it tags the partial records, which are never
+// cleared.  Epoch 0 (a call captured into a graph) tags them by the rows'
+// counters in the workspace instead, which the kernels advance.  With `ngram` (rows > 0, t >= n) the launch also applies the
 // n-gram bans.
 // `path` is the decomposition choose_attn_path gave for the call.
 hipError_t launch_cross_attn(const void *q, const void *K, const void *V,
@@ -74,7 +76,10 @@ hipError_t launch_ngram_block(const int32_t *tokens, int ld_tokens, int rows, in
 
 // Beam selection: vocabulary slices per hypothesis row, the most candidates
 // one source's ranking takes (k * slices * c) and the most record words it
-// reads (k * slices * (2 + 2c)), and the workspace in 64-bit words.  Record words carry the low 32 bits of `epoch` as their tag.
+// reads (k * slices * (2 + 2c)), and the workspace in 64-bit words (the
+// records, then one counter per source).  Record words carry `epoch` (in [1,
+// 2^31)) as their tag, or, with epoch 0 (a captured call), the source's
+// counter with bit 31 set.
 int beam_select_slices(int rows, int V, int k, int c);
 int beam_select_max_candidates();
 int beam_select_max_record_words();

@@ -91,13 +91,15 @@ def test_cross_attn_empty_problems_return_ok_without_launch():
 def test_workspace_bytes():
     f = N.lib().fs_beam_cross_attn_workspace_bytes
     assert f(0, 4, 16, 1024, 64, N.FS_BF16) == 0
-    assert f(2, 4, 2, 0, 16, N.FS_F32) == 2 * 2 * 4 * 4 * 18 * 8   # S = 0: one empty chunk column of 4 tiles
+    # S = 0: one empty chunk column of 4 tiles, and a counter per (b, h)
+    assert f(2, 4, 2, 0, 16, N.FS_F32) == 2 * 2 * 4 * 4 * 18 * 8 + 2 * 2 * 8
     assert f(2, 4, 2, 64, 48, N.FS_F32) == 2**64 - 1
     assert f(-1, 4, 2, 64, 16, N.FS_F32) == 2**64 - 1
     # per (b, h, 64-key tile): k * (D + 2) 8-byte tagged partials (tiles of
-    # four 256-key chunks at D = 64, bf16)
+    # four 256-key chunks at D = 64, bf16), then one 8-byte counter per (b, h)
+    # for captured calls
     a = f(32, 4, 16, 1024, 64, N.FS_BF16)
-    assert a == 32 * 16 * 16 * 4 * 66 * 8
+    assert a == 32 * 16 * 16 * 4 * 66 * 8 + 32 * 16 * 8
     assert f(64, 4, 16, 1024, 64, N.FS_BF16) == 2 * a
     assert f(32, 4, 16, 1025, 64, N.FS_BF16) > a
     assert f(32, 4, 16, 1023, 64, N.FS_BF16) == a
@@ -192,7 +194,8 @@ def test_select_rejects(kw, status, needle):
 def test_select_workspace_bytes_and_empty_batch():
     f = N.lib().fs_beam_select_workspace_bytes
     assert f(0, 4, 100, 8) == 0
-    assert f(2, 4, 100, 8) == 2 * 4 * 1 * (2 + 2 * 8) * 8      # one slice per row at V = 100
+    # one slice per row at V = 100, then one counter per source
+    assert f(2, 4, 100, 8) == 2 * 4 * 1 * (2 + 2 * 8) * 8 + 2 * 8
     assert f(2, 17, 100, 8) == ctypes.c_size_t(-1).value
     assert select(B=0, logits=None, bs=None, tokens=None, os=None, ob=None, ot=None, ws=None, wsb=0) == N.FS_OK
 
