@@ -249,7 +249,7 @@ struct MergeLds {
     unsigned long long best[16];
     unsigned long long hc;
     uint32_t w32[kMergeWords];
-    float lse[16], bsc[16];
+    float bsc[16];
     int stale, nsurv;
 };
 union SelectLds {
@@ -580,7 +580,7 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
                              int c, int NS, unsigned long long tag)
 {
     uint32_t *w32 = L.w32;
-    float *lse = L.lse, *bsc = L.bsc;
+    float *bsc = L.bsc;
     unsigned long long *keys = L.keys, *surv = L.surv, *best = L.best;
     int &stale = L.stale;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
@@ -593,7 +593,10 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
         L.hc = 0ull;
     }
     if (tid < 16) best[tid] = 0ull;
-    const float my_bs = tid < k ? beam_scores[(size_t)b * k + tid] : 0.f;
+    if (tid < k) bsc[tid] = beam_scores[(size_t)b * k + tid];
+    // the survivors' array holds 0 past its last entry (a 0 key ranks below
+    // every other), so no entry needs clearing after the packing
+    for (int e = tid; e < kMergeCap + 2; e += kThreads) surv[e] = 0ull;
     constexpr int kPerThread = kMergeWords / kThreads;
     unsigned long long wv[kPerThread];
 #pragma unroll
@@ -624,65 +627,47 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
     }
     __syncthreads();
     if (old) stale = 1;
-    // lse of each row: the slices in order
-    if (tid < k) {
-        // four slices per step, their reads issued together
-        const uint32_t *rw = w32 + tid * NS * W;
-        float M = -INFINITY;
-        int s = 0;
-        for (; s + 4 <= NS; s += 4) {
-            float q[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) q[u] = __uint_as_float(rw[(s + u) * W]);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) M = fmaxf(M, q[u]);
-        }
-        for (; s < NS; ++s) M = fmaxf(M, __uint_as_float(rw[s * W]));
-        float S = 0.f;
-        s = 0;
-        for (; s + 4 <= NS; s += 4) {
-            float ms[4], ss[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                ms[u] = __uint_as_float(rw[(s + u) * W]);
-                ss[u] = __uint_as_float(rw[(s + u) * W + 1]);
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                S += ms[u] == -INFINITY ? 0.f : ss[u] * __builtin_amdgcn_exp2f((ms[u] - M) * 1.4426950408889634f);
-        }
-        for (; s < NS; ++s) {
-            const float ms = __uint_as_float(rw[s * W]);
-            const float ss = __uint_as_float(rw[s * W + 1]);
-            S += ms == -INFINITY ? 0.f : ss * __builtin_amdgcn_exp2f((ms - M) * 1.4426950408889634f);
-        }
-        lse[tid] = M == -INFINITY ? -INFINITY : M + logf(S);
-        bsc[tid] = my_bs;
-    }
-    __syncthreads();
-    // every slice candidate, scored
+    // Every slice candidate, scored; each thread takes its row's lse from the
+    // row's slice records (the maximum, then the rescaled sums in slice
+    // order).  Keys are stored position-major, key (j, record q) at
+    // j * nrec + q, so the records' heads (j = 0) are the first nrec keys.
     const int ncand = k * NS * c;
+    const int nrec = k * NS;
+    constexpr float kL2e = 1.4426950408889634f;
     for (int e = tid; e < ncand; e += kThreads) {
         const int i = e / (NS * c), rem = e - i * NS * c, s = rem / c, j = rem - s * c;
-        const int base = (i * NS + s) * W;
-        const float x = __uint_as_float(w32[base + 2 + j]);
-        const uint32_t v = w32[base + 2 + c + j];
-        const float L = lse[i];
-        const float sc = (L == -INFINITY || x == -INFINITY) ? -INFINITY : bsc[i] + (x - L);
+        const uint32_t *rw = w32 + i * NS * W;
+        float M = -INFINITY;
+        for (int u = 0; u < NS; ++u) M = fmaxf(M, __uint_as_float(rw[u * W]));
+        float S = 0.f;
+        for (int u = 0; u < NS; ++u) {
+            const float ms = __uint_as_float(rw[u * W]);
+            const float ss = __uint_as_float(rw[u * W + 1]);
+            S += ms == -INFINITY ? 0.f : ss * __builtin_amdgcn_exp2f((ms - M) * kL2e);
+        }
+        const float lr = M == -INFINITY ? -INFINITY : M + logf(S);
+        const float x = __uint_as_float(rw[s * W + 2 + j]);
+        const uint32_t v = rw[s * W + 2 + c + j];
+        const float sc = (lr == -INFINITY || x == -INFINITY) ? -INFINITY : bsc[i] + (x - lr);
         // an empty slot (v = ~0) ranks below every candidate
-        keys[e] = v == 0xffffffffu ? 0ull : make_key(sc, (uint32_t)i * (uint32_t)V + v);
+        keys[j * nrec + i * NS + s] = v == 0xffffffffu ? 0ull : make_key(sc, (uint32_t)i * (uint32_t)V + v);
     }
     __syncthreads();
     // Prune: the heads (first candidates) of the k * NS records are distinct
     // candidates, so no candidate below the c-th largest head is among the c
     // best.  The heads are ranked among themselves, the candidates at or
     // above that head are packed, and only they are ranked.
-    const int nrec = k * NS;
     if (nrec >= c) {
+        const ulonglong2 *h2 = reinterpret_cast<const ulonglong2 *>(keys);
         for (int q = tid; q < nrec; q += kThreads) {
-            const unsigned long long hq = keys[q * c];
+            const unsigned long long hq = keys[q];
             int rank = 0;
-            for (int q2 = 0; q2 < nrec; ++q2) rank += keys[q2 * c] > hq;
+            int q2 = 0;
+            for (; 2 * q2 + 1 < nrec; ++q2) {
+                const ulonglong2 o = h2[q2];
+                rank += (o.x > hq) + (o.y > hq);
+            }
+            if (2 * q2 < nrec) rank += keys[2 * q2] > hq;
             if (rank == c - 1) L.hc = hq;   // heads other than 0 are distinct
         }
         __syncthreads();
@@ -702,8 +687,6 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
     }
     __syncthreads();
     const int ns = L.nsurv;
-    if (tid == 0) surv[ns] = 0ull;
-    __syncthreads();
     rank_top_keys(surv, ns, c, best);
     __syncthreads();
     if (tid < c) {
