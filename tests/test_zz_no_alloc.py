@@ -73,3 +73,57 @@ def test_noalloc_refuses_records_beyond_the_scratch_array():
     st = lib.fs_beam_decode_step_noalloc(fake, fake * 2, fake * 3, fake * 4, fake * 5, 1, 8, 127, 8192, 128,
                                          N.FS_BF16, fake * 6, 8, 8, 3, fake * 7, 100, None)
     assert st == N.FS_ERR_UNSUPPORTED and "scratch array" in N.last_error()
+
+
+def test_noalloc_step_replays_from_a_graph():
+    """The no-allocation step captured into a HIP graph (its split-KV records
+    in the library's scratch array, tagged by the array's counters): every
+    replay, on inputs refreshed in place, gives the bits of the workspace
+    step run eagerly on the same inputs."""
+    dev = device()
+    rng = np.random.default_rng(23)
+    B, k, H, S, D, t, n, vocab = 3, 4, 4, 900, 64, 40, 3, 300
+    q = torch.empty((B, k, H, D), dtype=torch.bfloat16, device=dev)
+    K = torch.empty((B, H, S, D), dtype=torch.bfloat16, device=dev)
+    V = torch.empty_like(K)
+    lens = torch.empty((B,), dtype=torch.int32, device=dev)
+    tok = torch.empty((B * k, t), dtype=torch.int32, device=dev)
+    lg = torch.empty((B * k, vocab), dtype=torch.float32, device=dev)
+    out = torch.empty_like(q)
+
+    def fill():
+        d = case(rng, B, k, H, S, D, t, vocab)
+        for dst, key in ((q, "q"), (K, "K"), (V, "V"), (lens, "src_len"), (tok, "tokens"), (lg, "logits")):
+            dst.copy_(to_dev(d[key]))
+        return d
+
+    def noalloc_step():
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        st = N.lib().fs_beam_decode_step_noalloc(
+            q.data_ptr(), K.data_ptr(), V.data_ptr(), lens.data_ptr(), out.data_ptr(), B, k, H, S, D, N.FS_BF16,
+            tok.data_ptr(), t, t, n, lg.data_ptr(), vocab, stream)
+        assert st == N.FS_OK, N.last_error()
+
+    fill()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        noalloc_step()
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    say("[noalloc] capture the no-allocation step")
+    with torch.cuda.graph(g):
+        noalloc_step()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        say(f"[noalloc] replay {rep}")
+        d = fill()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (bits(out).copy(), bits(lg).copy())
+        ref, _ = run_both(d)
+        assert np.array_equal(got[0], ref[0]), f"attention bits, replay {rep}"
+        assert np.array_equal(got[1], ref[1]), f"n-gram bits, replay {rep}"
