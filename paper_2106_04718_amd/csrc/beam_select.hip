@@ -420,11 +420,15 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     {
         const unsigned long long mine = bkey[lane];
         const ulonglong2 *b2 = reinterpret_cast<const ulonglong2 *>(bkey);
+        // four reads in flight at a time
         int rank = 0;
 #pragma unroll
-        for (int q = 0; q < kWave / 2; ++q) {
-            const ulonglong2 o = b2[q];
-            rank += (o.x > mine) + (o.y > mine);
+        for (int q0 = 0; q0 < kWave / 2; q0 += 4) {
+            ulonglong2 o[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) o[u] = b2[q0 + u];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) rank += (o[u].x > mine) + (o[u].y > mine);
         }
         const unsigned long long at = __builtin_amdgcn_ballot_w64(rank == c - 1);
         const int src = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(at));   // one lane: the keys are distinct
