@@ -299,6 +299,24 @@ enum {
 int fs_set_tuning(int knob, int value);
 
 /*
+ * Workgroup timelines, for measurement (not a method of the paper).  A
+ * library built with tracing (build.py: build(trace=True), which compiles
+ * every kernel with FS_TRACE=1) makes the attention kernels that take one
+ * workgroup per (source, head) row and the selection kernel write, for
+ * every workgroup g of each later launch, 8 64-bit words at buffer[8 g ..]
+ * (clock stamps of the 100 MHz s_memrealtime counter, the hardware ids of
+ * the compute unit, and counts; trace.h and the kernels list each word).
+ * Workgroups past bytes / 64 write nothing.  NULL stops tracing.  The
+ * buffer is device memory the caller owns; launches that overlap write
+ * the same words.
+ * Errors: FS_ERR_UNSUPPORTED in a library built without tracing (every
+ * normal build: its kernels contain no tracing code); FS_ERR_INVALID_ARG
+ * for a null buffer with bytes > 0 or one not 8-byte aligned; FS_ERR_HIP if
+ * the device symbol cannot be set.
+ */
+int fs_trace_set(void *buffer, size_t bytes);
+
+/*
  * Workspace, in bytes, that fs_beam_select needs for these sizes (per
  * (hypothesis, vocabulary slice) partial records, then a counter per source
  * for captured calls).  Zero-fill it before its

@@ -41,6 +41,7 @@ SIGNATURES = [
     ("fs_beam_decode_step", _c_int,
      [_vp] * 5 + [_c_int] * 6 + [_vp] + [_c_int] * 3 + [_vp, _c_int, _vp, _c_size, _vp]),
     ("fs_set_tuning", _c_int, [_c_int, _c_int]),
+    ("fs_trace_set", _c_int, [_vp, _c_size]),
     ("fs_beam_decode_step_noalloc", _c_int,
      [_vp] * 5 + [_c_int] * 6 + [_vp] + [_c_int] * 3 + [_vp, _c_int, _vp]),
     ("fs_beam_select_workspace_bytes", _c_size, [_c_int] * 4),

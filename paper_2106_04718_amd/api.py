@@ -185,6 +185,19 @@ def set_tuning(knob: int, value: int) -> int:
     return prev
 
 
+def trace_set(buffer: torch.Tensor | None) -> None:
+    """fs_trace_set: in a library built with workgroup tracing
+    (``build(trace=True)``), the device buffer the attention and selection
+    kernels write their workgroup timelines to (8 int64 words per
+    workgroup); None stops tracing.  Raises in other builds."""
+    if buffer is None:
+        st = _N.lib().fs_trace_set(None, 0)
+    else:
+        _need_cuda("buffer", buffer)
+        st = _N.lib().fs_trace_set(buffer.data_ptr(), buffer.numel() * buffer.element_size())
+    _N.check(st)
+
+
 @contextlib.contextmanager
 def attn_path(name: str):
     """Force one decomposition of the attention calls inside the block

@@ -7,6 +7,11 @@ pass warns that it does not know that feature, which is harmless.
 The CPython marshalling module (csrc/pyext.c, plain C) is then compiled with
 gcc and linked against the library.
 
+``build(trace=True)`` (``--trace``) compiles every source with FS_TRACE=1: the
+attention and selection kernels then write per-workgroup timelines to a
+buffer set with fs_trace_set (for measurements of where a launch spends its
+time; a plain ``build()`` restores the normal kernels).
+
 ``build(sanitize=True)`` (``python -m paper_2106_04718_amd.build --sanitize``)
 instruments the host code of every source with AddressSanitizer and
 UndefinedBehaviorSanitizer (``-Xarch_host``: device code is built as usual),
@@ -64,10 +69,10 @@ def sanitizer_runtime() -> str:
                           capture_output=True, text=True).stdout.strip()
 
 
-def _compile(src: str, verbose: bool, sanitize: bool = False) -> pathlib.Path:
+def _compile(src: str, verbose: bool, sanitize: bool = False, trace: bool = False) -> pathlib.Path:
     obj = BUILD / (src + ".o")
-    cmd = [hipcc(), *COMMON, *(SANITIZE_HOST if sanitize else []), "-x", "hip", "-c", str(CSRC / src),
-           "-o", str(obj)]
+    cmd = [hipcc(), *COMMON, *(SANITIZE_HOST if sanitize else []), *(["-DFS_TRACE=1"] if trace else []),
+           "-x", "hip", "-c", str(CSRC / src), "-o", str(obj)]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -80,10 +85,10 @@ def _compile(src: str, verbose: bool, sanitize: bool = False) -> pathlib.Path:
     return obj
 
 
-def build(verbose: bool = False, sanitize: bool = False) -> pathlib.Path:
+def build(verbose: bool = False, sanitize: bool = False, trace: bool = False) -> pathlib.Path:
     BUILD.mkdir(exist_ok=True)
     with concurrent.futures.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose, sanitize), SOURCES))
+        objs = list(ex.map(lambda s: _compile(s, verbose, sanitize, trace), SOURCES))
     tmp = str(LIB) + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-Wl,-soname,libfastseq_hip.so",
            *(SANITIZE_LINK if sanitize else []), *map(str, objs), "-o", tmp]
@@ -112,4 +117,4 @@ def build_ext(verbose: bool = False, sanitize: bool = False) -> pathlib.Path:
 
 if __name__ == "__main__":
     import sys
-    print(build(verbose=True, sanitize="--sanitize" in sys.argv[1:]))
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv[1:], trace="--trace" in sys.argv[1:]))

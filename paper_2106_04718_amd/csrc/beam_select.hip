@@ -41,6 +41,7 @@
 
 
 #include "launch.h"
+#include "trace.h"
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -58,6 +59,18 @@ constexpr int kMaxSpins = 1 << 14;       // bounded re-reads of a record word (a
 constexpr int kNMax = 8;                 // n-gram sizes whose first window is loaded ahead
 constexpr int kWaves = kThreads / kWave;
 constexpr int kBlocks = kWave / kWaves;   // threshold blocks per wave: 64 in a workgroup
+
+#if FS_TRACE
+__device__ trace::Target g_trace{nullptr, 0};
+#endif
+// this workgroup's timeline words in a trace build, else null
+__device__ __forceinline__ unsigned long long *trace_slot() {
+#if FS_TRACE
+    return trace::slot(g_trace);
+#else
+    return nullptr;
+#endif
+}
 
 // Order-preserving 32-bit image of a float (larger value, larger image);
 // -0 is taken as +0.
@@ -280,6 +293,10 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     float *wm = L.wm, *ws = L.ws;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+    // trace words: 0 start, 1 data in, 2 threshold, 3 collected, 4 end,
+    // 5 hardware ids, 6 candidates, 7 = 0 (a slice)
+    unsigned long long *trs = trace_slot();
+    trace::stamp(trs, 0);
     const int v0 = s * SL, v1 = min(V, v0 + SL), len = max(0, v1 - v0);
     const float *x = logits + (size_t)r * V + v0;
     const int a = (int)((reinterpret_cast<uintptr_t>(x) >> 2) & 3);
@@ -370,6 +387,10 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     }
     // the wave's (max, sum of exp) over every logit, banned or not
     const float mw = wave_max_f(m);
+    if (trs) {
+        asm volatile("" ::"v"(mw));   // the stamp after the data
+        trace::stamp(trs, 1);
+    }
     float sum = 0.f;
     if (mw != -INFINITY) {
         const float sh = mw * kLog2e;
@@ -434,6 +455,10 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
         const int src = __builtin_amdgcn_readfirstlane((int)__builtin_ctzll(at));   // one lane: the keys are distinct
         tau = unordered((uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(mine >> 32), src));
     }
+    if (trs) {
+        asm volatile("" ::"v"(tau));
+        trace::stamp(trs, 2);
+    }
 
     // Collect the positions at or above tau as keys.  Positions outside the
     // slice hold -inf, below a finite tau; for tau = -inf they become NaN
@@ -475,6 +500,8 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
     }
     lds_barrier();
     const int total = L.ncand;
+    trace::stamp(trs, 3);
+    trace::put(trs, 6, (unsigned long long)total);
     unsigned long long *rec = part + ((size_t)r * NS + s) * rec_words(c);
     if (total <= kWave) {
         // Few candidates: wave 0 ranks them in registers and writes the
@@ -573,6 +600,9 @@ __device__ void select_slice(SliceLds &L, const float *__restrict__ logits, cons
         store_word(rec, tag, __float_as_uint(M));
         store_word(rec + 1, tag, __float_as_uint(S));
     }
+    trace::stamp(trs, 4);
+    trace::put(trs, 5, trace::where());
+    trace::put(trs, 7, 0);
 }
 
 // Merger of source b: reads the k * NS records of its rows into LDS (every
@@ -591,6 +621,10 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
     const int W = rec_words(c);
     const int nw = k * NS * W;
     const unsigned long long *recs = part + (size_t)b * k * NS * W;
+    // trace words: 0 start, 1 records in, 4 end, 5 hardware ids,
+    // 6 survivors, 7 = 1 (a merger)
+    unsigned long long *trs = trace_slot();
+    trace::stamp(trs, 0);
     if (tid == 0) {
         stale = 0;
         L.nsurv = 0;
@@ -630,6 +664,7 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
         if (e < nw) w32[e] = (uint32_t)wv[q];
     }
     __syncthreads();
+    trace::stamp(trs, 1);
     if (old) stale = 1;
     // Every slice candidate, scored; each thread takes its row's lse from the
     // row's slice records (the maximum, then the rescaled sums in slice
@@ -701,6 +736,10 @@ __device__ void select_merge(MergeLds &L, const float *__restrict__ beam_scores,
         out_beam[(size_t)b * c + tid] = bad ? -1 : (int32_t)(f / (uint32_t)V);
         out_token[(size_t)b * c + tid] = bad ? -1 : (int32_t)(f % (uint32_t)V);
     }
+    trace::stamp(trs, 4);
+    trace::put(trs, 5, trace::where());
+    trace::put(trs, 6, (unsigned long long)ns);
+    trace::put(trs, 7, 1);
 }
 
 __global__ __launch_bounds__(kThreads) void beam_select_kernel(
@@ -732,6 +771,17 @@ __global__ __launch_bounds__(kThreads) void beam_select_kernel(
 namespace {
 std::atomic<int> g_slices_override{0};
 }  // namespace
+
+hipError_t set_select_trace(unsigned long long *buf, unsigned int cap) {
+#if FS_TRACE
+    const trace::Target t{buf, cap};
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_trace), &t, sizeof(t));
+#else
+    (void)buf;
+    (void)cap;
+    return hipErrorNotSupported;
+#endif
+}
 
 int set_select_slices_override(int slices) {
     return g_slices_override.exchange(slices > 0 ? slices : 0, std::memory_order_relaxed);

@@ -409,6 +409,22 @@ int fs_beam_decode_step_noalloc(const void *q, const void *K, const void *V, con
                        nullptr, 0, stream, true);
 }
 
+int fs_trace_set(void *buffer, size_t bytes)
+{
+    g_last_error.clear();
+    if (bytes > 0 && !buffer) return fail(FS_ERR_INVALID_ARG, "null trace buffer of %zu bytes", bytes);
+    if (buffer && !aligned(buffer, 8)) return fail(FS_ERR_INVALID_ARG, "trace buffer must be 8-byte aligned");
+    const size_t cap = buffer ? bytes / 64 : 0;
+    unsigned long long *buf = cap ? static_cast<unsigned long long *>(buffer) : nullptr;
+    const unsigned int c = cap > 0xffffffffu ? 0xffffffffu : (unsigned int)cap;
+    hipError_t e = fs::set_attn_trace(buf, c);
+    if (e == hipErrorNotSupported)
+        return fail(FS_ERR_UNSUPPORTED, "this library was built without workgroup tracing (build with trace=True)");
+    if (e == hipSuccess) e = fs::set_select_trace(buf, c);
+    if (e != hipSuccess) return hip_fail(e, "fs_trace_set");
+    return FS_OK;
+}
+
 int fs_set_tuning(int knob, int value)
 {
     switch (knob) {

@@ -44,6 +44,7 @@
 
 #include "launch.h"
 #include "ngram_row.h"
+#include "trace.h"
 
 namespace fs {
 namespace {
@@ -256,6 +257,18 @@ __device__ __forceinline__ void group_reduce_scatter(float (&d)[NI][KB], int sub
 
 // Index of this wave in its workgroup, as a wave-uniform (scalar) value, so
 // that branches on it are uniform and each side keeps its own registers.
+#if FS_TRACE
+__device__ trace::Target g_trace{nullptr, 0};
+#endif
+// this workgroup's timeline words in a trace build, else null
+__device__ __forceinline__ unsigned long long *trace_slot() {
+#if FS_TRACE
+    return trace::slot(g_trace);
+#else
+    return nullptr;
+#endif
+}
+
 __device__ __forceinline__ int wave_id() {
     return __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
 }
@@ -1107,6 +1120,9 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
     }
     const int bh = blockIdx.x - ngj.blocks;
     if (bh >= n_bh) return;
+    // trace words: 0 start, 1 end, 2 hardware ids, 3 row, 4 jobs, 5 first round folded
+    unsigned long long *trs = trace_slot();
+    trace::stamp(trs, 0);
     const int b = bh / H;
     const int h = bh - b * H;
     const int L = min(max(src_len[b], 0), S);
@@ -1208,6 +1224,7 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
             }
         }
         __syncthreads();
+        if (j0 == 0) trace::stamp(trs, 5);
     }
     if (ng) {
 #pragma unroll
@@ -1228,6 +1245,10 @@ __global__ __launch_bounds__(kBlock * P) void attn_whole_kernel(
             store_out<BF16>(out, obase + (size_t)i * H * D + d, any ? Ra[p] / Rl[p] : 0.f);  // no key: zero row
         }
     }
+    trace::stamp(trs, 1);
+    trace::put(trs, 2, trace::where());
+    trace::put(trs, 3, (unsigned long long)bh);
+    trace::put(trs, 4, (unsigned long long)njobs);
 }
 
 // Launch arguments shared by both entry points.  For the encoder-decoder
@@ -1350,6 +1371,17 @@ hipError_t launch_d(const AttnArgs &a)
 namespace {
 std::atomic<int> g_path_override{0};
 }  // namespace
+
+hipError_t set_attn_trace(unsigned long long *buf, unsigned int cap) {
+#if FS_TRACE
+    const trace::Target t{buf, cap};
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_trace), &t, sizeof(t));
+#else
+    (void)buf;
+    (void)cap;
+    return hipErrorNotSupported;
+#endif
+}
 
 AttnPath set_attn_path_override(AttnPath p) {
     return static_cast<AttnPath>(g_path_override.exchange(static_cast<int>(p), std::memory_order_relaxed));

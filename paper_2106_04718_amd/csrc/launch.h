@@ -31,6 +31,12 @@ enum class AttnPath { kAuto = 0, kSplit, kWhole1, kWhole2, kWhole4 };
 // forced with set_attn_path_override.
 AttnPath choose_attn_path(int n_bh, int jobs_max);
 
+// Workgroup timelines of trace builds (trace.h): the buffer the attention
+// kernels and the selection kernel write (8 words per workgroup, `cap`
+// workgroups; null: none).  hipErrorNotSupported in other builds.
+hipError_t set_attn_trace(unsigned long long *buf, unsigned int cap);
+hipError_t set_select_trace(unsigned long long *buf, unsigned int cap);
+
 // Process-wide overrides of the size rules, for tests and measurements
 // (fs_set_tuning).  kAuto / 0 restore the rules; each returns the previous value.
 AttnPath set_attn_path_override(AttnPath p);

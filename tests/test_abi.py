@@ -399,3 +399,11 @@ def test_postproc_rejects_bad_arguments_before_any_hip_call():
     assert lib.fs_postproc_flush(None) == N.FS_ERR_INVALID_ARG
     assert lib.fs_postproc_output(None, None, 0) == 0
     lib.fs_postproc_destroy(None)
+
+
+def test_trace_set_needs_a_trace_build():
+    lib = N.lib()
+    assert lib.fs_trace_set(None, 64) == N.FS_ERR_INVALID_ARG and "null trace buffer" in N.last_error()
+    assert lib.fs_trace_set(FAKE + 4, 64) == N.FS_ERR_INVALID_ARG and "aligned" in N.last_error()
+    # a normal build holds no tracing code: refused before any HIP call
+    assert lib.fs_trace_set(None, 0) == N.FS_ERR_UNSUPPORTED and "without workgroup tracing" in N.last_error()
